@@ -1,0 +1,53 @@
+"""One layer of the method's video hot path, composed from the oracle steps,
+and its exact work count (Sec. 4.4, Eq. (16)).
+
+Test infrastructure only; see the package docstring.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .saliency import cross_scores, token_to_block_saliency
+from .selection import select_protected
+from .mask import block_mask
+from .attention import masked_attention
+
+
+def protected_sparse_layer(q_v, k_v, v_v, q_a, k_a, scale, block, k_keep,
+                           k_prot, with_audio=True):
+    """Saliency (Eq. (1)-(2)), protected blocks (Eq. (8)), protected block
+    mask (Eq. (9)) and protected sparse attention (Eq. (10)/(11))."""
+    s_v, s_a = cross_scores(q_a, k_v, scale,
+                            q_v if with_audio else None,
+                            k_a if with_audio else None)
+    s_blk = token_to_block_saliency(s_v, block)
+    prot_idx, prot_flag = select_protected(s_blk, k_prot)
+    m = block_mask(q_v, k_v, scale, block, k_keep, prot_flag)
+    O, lse = masked_attention(q_v, k_v, v_v, scale, block, m["kv_idx"],
+                              m["kv_cnt"])
+    return {"sal_v_tok": s_v, "sal_v_blk": s_blk, "sal_a_tok": s_a,
+            "prot_idx": prot_idx, "prot_flag": prot_flag, **m,
+            "O": O, "lse": lse}
+
+
+def computed_flops(kv_idx, kv_cnt, N, block, d):
+    """Attention flops actually computed over kept pairs:
+    ``4 * d * sum_r rows(r) * sum_{c in keep(r)} cols(c)`` (QK^T and PV, two
+    flops per multiply-add), the exact form of Eq. (16)."""
+    kv_idx = np.asarray(kv_idx)
+    kv_cnt = np.asarray(kv_cnt)
+    B, H, n_b = kv_cnt.shape
+    lens = np.array([min((c + 1) * block, N) - c * block for c in range(n_b)],
+                    dtype=np.int64)
+    total = 0
+    for b in range(B):
+        for h in range(H):
+            for r in range(n_b):
+                cols = kv_idx[b, h, r, :kv_cnt[b, h, r]]
+                total += int(lens[r]) * int(lens[cols].sum())
+    return 4 * d * total
+
+
+def dense_flops(B, H, N, d):
+    """Flops of dense attention, Eq. (5): ``4 * B * H * N^2 * d``."""
+    return 4 * B * H * N * N * d
