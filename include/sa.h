@@ -1,0 +1,183 @@
+/*
+ * sa.h -- C ABI of the protected block-sparse video attention library
+ * (libsa.so, MI355X / gfx950).
+ *
+ * The library implements one layer of the video hot path of
+ * "Efficient Audio-Visual Generation via Synchrony-Aware Cross-Modal Sparse
+ * Attention":
+ *   1. sa_cross_scores      -- bidirectional audio-video cross-attention
+ *                              saliency (Sec. 4.1, Eq. (1)-(2) and the
+ *                              reverse direction stated after Eq. (2));
+ *   2. sa_select_protected  -- protected query blocks by top-k of the block
+ *                              saliency (Sec. 4.1 Eq. (3), Sec. 4.2 Eq. (8));
+ *   3. sa_build_block_mask  -- sparse pattern S_m as pooled-QK block top-k,
+ *                              with full rows for protected query blocks
+ *                              (Sec. 4.2, Eq. (6) and (9));
+ *   4. sa_sparse_attention  -- block-sparse flash attention over the
+ *                              compacted key-block lists (Sec. 4.2,
+ *                              Eq. (10)/(11); Eq. (5) when every list is full).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are DEVICE pointers owned by the caller, contiguous, row-major
+ *   [B, H, L, d] with d innermost, 16-byte aligned.  Q/K/V/O of one call share
+ *   one dtype (SA_BF16 or SA_F32).  The library never allocates, frees or
+ *   copies to the host.
+ * - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
+ *   NULL = the default stream) and never synchronise the host.
+ * - Return value: SA_OK or an SA_ERR_* code.  On any error nothing has been
+ *   launched and nothing written; sa_last_error() gives a message
+ *   (thread-local, valid until the next call on the same thread).
+ *   SA_ERR_HIP reports a failed kernel launch (hipGetLastError).
+ * - Budgets are plain integers; the caller computes ceil(ratio * count).
+ * - Supported sizes: d in {64, 128}; block in {64, 128};
+ *   1 <= n_b = ceil(L_v / block) <= 2048; L_a >= 1.
+ * - Results are bit-reproducible run to run (no floating-point atomics).
+ * - Scratch memory ("workspace") is passed by the caller; its minimum size is
+ *   sa_workspace_size(call, ...).  A smaller ws_bytes fails with
+ *   SA_ERR_WORKSPACE.
+ */
+#ifndef SA_H_
+#define SA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  SA_OK = 0,
+  SA_ERR_INVALID_ARG = 1,  /* null pointer, bad size, bad budget, alignment */
+  SA_ERR_UNSUPPORTED = 2,  /* d, block or dtype outside the supported set */
+  SA_ERR_WORKSPACE = 3,    /* ws_bytes below sa_workspace_size(...) */
+  SA_ERR_HIP = 4           /* a kernel launch failed */
+};
+
+enum { SA_BF16 = 0, SA_F32 = 1 };
+
+enum {
+  SA_CALL_CROSS_SCORES = 0,
+  SA_CALL_BUILD_BLOCK_MASK = 1,
+  SA_CALL_SPARSE_ATTENTION = 2,
+  SA_CALL_SELECT_PROTECTED = 3
+};
+
+/*
+ * sa_cross_scores -- token and block saliency of one cross-attention layer.
+ *
+ * Sec. 4.1, Eq. (1): A^{a->v} = softmax(Q^a (K^v)^T * scale) over all L_v
+ * video keys, per batch item and head.  Eq. (2): the video-token saliency is
+ * the column mass of A^{a->v} summed over audio queries and heads, with Norm
+ * taken as division by H * L_a (each softmax row sums to one, so the map sums
+ * to one per batch item).  The reverse direction (v->a, the sentence after
+ * Eq. (2)) gives the audio-token saliency with softmax over the L_a audio
+ * keys, summed over video queries and heads, divided by H * L_v.  The block
+ * saliency is the sum of the token saliency over each block of `block`
+ * consecutive video tokens (the last block may be shorter).
+ *
+ *   q_a        [B,H,L_a,d]  audio queries (required)
+ *   k_v        [B,H,L_v,d]  video keys (required)
+ *   q_v        [B,H,L_v,d]  video queries; NULL skips the v->a direction
+ *   k_a        [B,H,L_a,d]  audio keys; NULL iff q_v is NULL
+ *   scale      softmax scale (normally 1/sqrt(d)), finite and > 0
+ *   sal_v_tok  [B,L_v] f32 out, nullable
+ *   sal_v_blk  [B,n_b] f32 out, required
+ *   sal_a_tok  [B,L_a] f32 out, must be NULL iff q_v is NULL
+ *   accumulate 0: outputs are overwritten; 1: the new values are added to
+ *              what the outputs hold (sum over the layers of L_c)
+ *   ws         workspace of at least sa_workspace_size(SA_CALL_CROSS_SCORES)
+ */
+int sa_cross_scores(const void* q_a, const void* k_v, const void* q_v,
+                    const void* k_a, int B, int H, int L_v, int L_a, int d,
+                    int dtype, float scale, int block, float* sal_v_tok,
+                    float* sal_v_blk, float* sal_a_tok, int accumulate,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * sa_select_protected -- protected query blocks (Sec. 4.2, Eq. (8), at block
+ * granularity; Sec. 4.1, Eq. (3)).
+ *
+ * Per batch item, the k_prot blocks of largest sal_blk; equal scores are
+ * ordered by lower block index first.  The caller chooses which map is
+ * ranked (the current one, or the lagged cache of Eq. (4)).
+ *
+ *   sal_blk    [B,n_b] f32 in (finite values)
+ *   k_prot     0 <= k_prot <= n_b
+ *   prot_idx   [B,k_prot] i32 out in rank order, nullable
+ *   prot_flag  [B,n_b] u8 out, 1 = protected, required
+ */
+int sa_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
+                        int32_t* prot_idx, uint8_t* prot_flag, void* stream);
+
+/*
+ * sa_build_block_mask -- the protected block mask M~ of Eq. (9) as compacted
+ * key-block lists (Sec. 4.2, Eq. (6) and (9)).
+ *
+ * The sparse pattern S_m is pooled-QK block top-k: Q and K are averaged over
+ * each block of `block` tokens (the last block over its true length), the
+ * pooled score is G[r,c] = scale * qbar_r . kbar_c in fp32, and every query
+ * block r that is not protected keeps the k_keep key blocks of largest
+ * G[r,:] (equal scores: lower block index first).  A protected query block
+ * keeps every key block; protection adds rows only.
+ *
+ *   q_v, k_v   [B,H,L_v,d] video queries and keys
+ *   k_keep     1 <= k_keep <= n_b
+ *   prot_flag  [B,n_b] u8 (nonzero = protected), shared by all heads;
+ *              NULL = nothing protected
+ *   kv_idx     [B,H,n_b,n_b] i32 out: kept key blocks of each query block in
+ *              ascending order, first kv_cnt entries valid, the rest -1
+ *   kv_cnt     [B,H,n_b] i32 out
+ *   mask       [B,H,n_b,n_b] u8 out (1 = kept), nullable
+ *   scores     [B,H,n_b,n_b] f32 out: the pooled scores G, nullable
+ *   ws         workspace of at least sa_workspace_size(SA_CALL_BUILD_BLOCK_MASK)
+ */
+int sa_build_block_mask(const void* q_v, const void* k_v, int B, int H,
+                        int L_v, int d, int dtype, float scale, int block,
+                        int k_keep, const uint8_t* prot_flag, int32_t* kv_idx,
+                        int32_t* kv_cnt, uint8_t* mask, float* scores,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * sa_sparse_attention -- protected block-sparse attention (Sec. 4.2,
+ * Eq. (10) in its row form Eq. (11)).
+ *
+ * Query block r of head (b,h) attends to the tokens of key blocks
+ * kv_idx[b,h,r,0:kv_cnt[b,h,r]] with an exact softmax (non-causal); a full
+ * list gives dense attention, Eq. (5).  Keys past L do not exist.
+ *
+ *   q, k, v    [B,H,L,d] in dtype
+ *   o          [B,H,L,d] out in dtype (round to nearest even from fp32)
+ *   lse        [B,H,L] f32 out, natural-log log-sum-exp of the scaled
+ *              logits of each row, nullable
+ *   kv_idx     [B,H,n_b,n_b] i32; entries outside [0,n_b) are ignored
+ *   kv_cnt     [B,H,n_b] i32, clamped to [0,n_b]; a row with no valid entry
+ *              outputs zeros and lse = -inf
+ *   ws         workspace of at least sa_workspace_size(SA_CALL_SPARSE_ATTENTION)
+ */
+int sa_sparse_attention(const void* q, const void* k, const void* v, void* o,
+                        float* lse, int B, int H, int L, int d, int dtype,
+                        float scale, int block, const int32_t* kv_idx,
+                        const int32_t* kv_cnt, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/*
+ * Minimum workspace bytes of a call (SA_CALL_*) at the given sizes; L_a is
+ * read by SA_CALL_CROSS_SCORES only.  Returns 0 for sizes the call rejects.
+ * The figure covers both dtypes.
+ */
+size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d,
+                         int block);
+
+/* Message for the last non-OK return on this thread ("" if none). */
+const char* sa_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+int sa_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SA_H_ */

@@ -15,6 +15,8 @@ Readings taken where the paper is silent:
 """
 from __future__ import annotations
 
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 
@@ -25,7 +27,29 @@ def _softmax_rows(logits: np.ndarray) -> np.ndarray:
     return e / e.sum(axis=1, keepdims=True)
 
 
-def cross_scores(q_a, k_v, scale, q_v=None, k_a=None):
+def _column_mass(q, k, scale):
+    """Column sums of the row softmax of ``scale * q k^T`` (one head)."""
+    return _softmax_rows(scale * (q @ k.T)).sum(axis=0)
+
+
+def _direction(q, k, scale, workers):
+    """sum_h of the column mass, per batch item, heads added in order."""
+    B, H = q.shape[:2]
+    jobs = [(b, h) for b in range(B) for h in range(H)]
+    run = lambda bh: _column_mass(np.asarray(q[bh], dtype=np.float64),
+                                  np.asarray(k[bh], dtype=np.float64), scale)
+    if workers > 1:
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            cols = list(ex.map(run, jobs))
+    else:
+        cols = [run(bh) for bh in jobs]
+    out = np.zeros((B, k.shape[2]), dtype=np.float64)
+    for (b, h), c in zip(jobs, cols):
+        out[b] += c
+    return out
+
+
+def cross_scores(q_a, k_v, scale, q_v=None, k_a=None, workers=1):
     """Token saliency of both modalities for one layer.
 
     Eq. (1): ``A^{a->v} = softmax(Q^a (K^v)^T * scale)`` per batch item and
@@ -39,29 +63,17 @@ def cross_scores(q_a, k_v, scale, q_v=None, k_a=None):
         q_v: [B, H, N_v, d] video queries, k_a: [B, H, N_a, d] audio keys;
             both None to skip the reverse direction.
         scale: the softmax scale (1/sqrt(d_h)).
+        workers: heads evaluated concurrently (threads); the per-head terms
+            are still added in head order, so the result does not depend on it.
     Returns:
         (s_v [B, N_v], s_a [B, N_a] or None), float64, each row summing to 1.
     """
-    q_a = np.asarray(q_a, dtype=np.float64)
-    k_v = np.asarray(k_v, dtype=np.float64)
-    B, H, N_a, _ = q_a.shape
-    N_v = k_v.shape[2]
-    s_v = np.zeros((B, N_v), dtype=np.float64)
-    for b in range(B):
-        for h in range(H):
-            A = _softmax_rows(scale * (q_a[b, h] @ k_v[b, h].T))   # [N_a, N_v]
-            s_v[b] += A.sum(axis=0)
-    s_v /= H * N_a
+    H, N_a = q_a.shape[1], q_a.shape[2]
+    s_v = _direction(q_a, k_v, scale, workers) / (H * N_a)
     s_a = None
     if q_v is not None:
-        q_v = np.asarray(q_v, dtype=np.float64)
-        k_a = np.asarray(k_a, dtype=np.float64)
-        s_a = np.zeros((B, N_a), dtype=np.float64)
-        for b in range(B):
-            for h in range(H):
-                A = _softmax_rows(scale * (q_v[b, h] @ k_a[b, h].T))  # [N_v, N_a]
-                s_a[b] += A.sum(axis=0)
-        s_a /= H * N_v
+        N_v = q_v.shape[2]
+        s_a = _direction(q_v, k_a, scale, workers) / (H * N_v)
     return s_v, s_a
 
 

@@ -1,0 +1,16 @@
+"""Protected block-sparse video attention for MI355X (gfx950).
+
+The video hot path of "Efficient Audio-Visual Generation via Synchrony-Aware
+Cross-Modal Sparse Attention" (Sec. 4.1-4.2): cross-modal saliency, protected
+block selection, the protected pooled-QK block mask and block-sparse flash
+attention, implemented as hand-written HIP kernels behind a C ABI
+(``include/sa.h``, ``libsa.so``) with a thin ctypes binding.
+"""
+from .binding import (  # noqa: F401
+    SaError, lib, sa_build_block_mask, sa_cross_scores, sa_last_error,
+    sa_select_protected, sa_sparse_attention, sa_version, sa_workspace_size,
+    SA_BF16, SA_F32, SA_CALL_CROSS_SCORES, SA_CALL_BUILD_BLOCK_MASK,
+    SA_CALL_SPARSE_ATTENTION, SA_CALL_SELECT_PROTECTED, SA_OK,
+    SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP,
+)
+from .layer import protected_sparse_layer  # noqa: F401

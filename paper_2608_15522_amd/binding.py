@@ -1,0 +1,187 @@
+"""ctypes binding of libsa.so: argument marshalling only.
+
+Each function has the name of the C entry point it calls.  Torch tensors
+supply device pointers; ``torch.cuda.current_stream()`` supplies the HIP
+stream; outputs and the workspace that the caller does not pass are allocated
+with ``torch.empty`` (PyTorch is the device-memory allocator here).  All
+arithmetic runs in the library's kernels.  There is no fallback: if
+``libsa.so`` is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsa.so")
+
+SA_OK, SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP = range(5)
+SA_BF16, SA_F32 = 0, 1
+(SA_CALL_CROSS_SCORES, SA_CALL_BUILD_BLOCK_MASK, SA_CALL_SPARSE_ATTENTION,
+ SA_CALL_SELECT_PROTECTED) = range(4)
+
+# Every symbol the C header declares, with its ctypes signature.
+_VP, _I, _F, _SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+SIGNATURES = {
+    "sa_cross_scores": (_I, [_VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _I, _F, _I,
+                             _VP, _VP, _VP, _I, _VP, _SZ, _VP]),
+    "sa_select_protected": (_I, [_VP, _I, _I, _I, _VP, _VP, _VP]),
+    "sa_build_block_mask": (_I, [_VP, _VP, _I, _I, _I, _I, _I, _F, _I, _I, _VP,
+                                 _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "sa_sparse_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _F,
+                                 _I, _VP, _VP, _VP, _SZ, _VP]),
+    "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
+    "sa_last_error": (ctypes.c_char_p, []),
+    "sa_version": (_I, []),
+}
+
+
+class SaError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"[sa error {code}] {message}")
+        self.code = code
+
+
+_lib_handle = None
+
+
+def lib():
+    """The loaded library (loaded on first use; raises if it is not built)."""
+    global _lib_handle
+    if _lib_handle is None:
+        if not os.path.exists(LIB_PATH):
+            raise SaError(-1, f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2608_15522_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib_handle = handle
+    return _lib_handle
+
+
+def sa_last_error() -> str:
+    return lib().sa_last_error().decode()
+
+
+def sa_version() -> int:
+    return lib().sa_version()
+
+
+def _check(rc: int):
+    if rc != SA_OK:
+        raise SaError(rc, sa_last_error())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SA_BF16
+    if t.dtype == torch.float32:
+        return SA_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def sa_workspace_size(call: int, B: int, H: int, L_v: int, L_a: int, d: int,
+                      block: int) -> int:
+    return int(lib().sa_workspace_size(call, B, H, L_v, L_a, d, block))
+
+
+def _workspace(call, B, H, L_v, L_a, d, block, device, ws):
+    need = sa_workspace_size(call, B, H, L_v, L_a, d, block)
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return ws
+
+
+def sa_cross_scores(q_a, k_v, q_v, k_a, scale, block, *, sal_v_tok=None,
+                    sal_v_blk=None, sal_a_tok=None, accumulate=False,
+                    want_tok=True, ws=None):
+    """Token/block saliency; returns (sal_v_tok, sal_v_blk, sal_a_tok)."""
+    B, H, L_a, d = q_a.shape
+    L_v = k_v.shape[2]
+    n_b = -(-L_v // block)
+    dev = q_a.device
+    if sal_v_blk is None:
+        sal_v_blk = torch.empty(B, n_b, dtype=torch.float32, device=dev)
+    if sal_v_tok is None and want_tok:
+        sal_v_tok = torch.empty(B, L_v, dtype=torch.float32, device=dev)
+    if q_v is not None and sal_a_tok is None:
+        sal_a_tok = torch.empty(B, L_a, dtype=torch.float32, device=dev)
+    ws = _workspace(SA_CALL_CROSS_SCORES, B, H, L_v, L_a, d, block, dev, ws)
+    _check(lib().sa_cross_scores(
+        _ptr(q_a), _ptr(k_v), _ptr(q_v), _ptr(k_a), B, H, L_v, L_a, d,
+        _dtype_code(q_a), float(scale), block, _ptr(sal_v_tok), _ptr(sal_v_blk),
+        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), ws.numel(), _stream()))
+    return sal_v_tok, sal_v_blk, sal_a_tok
+
+
+def sa_select_protected(sal_blk, k_prot, *, prot_idx=None, prot_flag=None,
+                        want_idx=True):
+    """Protected blocks; returns (prot_idx [B,k_prot] i32, prot_flag [B,n_b] u8)."""
+    B, n_b = sal_blk.shape
+    dev = sal_blk.device
+    if prot_idx is None and want_idx:
+        prot_idx = torch.empty(B, max(k_prot, 0), dtype=torch.int32, device=dev)
+    if prot_flag is None:
+        prot_flag = torch.empty(B, n_b, dtype=torch.uint8, device=dev)
+    _check(lib().sa_select_protected(_ptr(sal_blk), B, n_b, int(k_prot),
+                                     _ptr(prot_idx) if k_prot > 0 else None,
+                                     _ptr(prot_flag), _stream()))
+    return prot_idx, prot_flag
+
+
+def sa_build_block_mask(q_v, k_v, scale, block, k_keep, prot_flag=None, *,
+                        kv_idx=None, kv_cnt=None, want_mask=False,
+                        want_scores=False, mask=None, scores=None, ws=None):
+    """Compacted protected block mask; returns (kv_idx, kv_cnt, mask, scores)."""
+    B, H, L_v, d = q_v.shape
+    n_b = -(-L_v // block)
+    dev = q_v.device
+    if kv_idx is None:
+        kv_idx = torch.empty(B, H, n_b, n_b, dtype=torch.int32, device=dev)
+    if kv_cnt is None:
+        kv_cnt = torch.empty(B, H, n_b, dtype=torch.int32, device=dev)
+    if mask is None and want_mask:
+        mask = torch.empty(B, H, n_b, n_b, dtype=torch.uint8, device=dev)
+    if scores is None and want_scores:
+        scores = torch.empty(B, H, n_b, n_b, dtype=torch.float32, device=dev)
+    ws = _workspace(SA_CALL_BUILD_BLOCK_MASK, B, H, L_v, 1, d, block, dev, ws)
+    _check(lib().sa_build_block_mask(
+        _ptr(q_v), _ptr(k_v), B, H, L_v, d, _dtype_code(q_v), float(scale), block,
+        int(k_keep), _ptr(prot_flag), _ptr(kv_idx), _ptr(kv_cnt), _ptr(mask),
+        _ptr(scores), _ptr(ws), ws.numel(), _stream()))
+    return kv_idx, kv_cnt, mask, scores
+
+
+def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
+                        lse=None, want_lse=False, ws=None):
+    """Block-sparse attention; returns (o, lse)."""
+    B, H, L, d = q.shape
+    dev = q.device
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(B, H, L, dtype=torch.float32, device=dev)
+    ws = _workspace(SA_CALL_SPARSE_ATTENTION, B, H, L, 1, d, block, dev, ws)
+    _check(lib().sa_sparse_attention(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
+        float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), ws.numel(),
+        _stream()))
+    return o, lse

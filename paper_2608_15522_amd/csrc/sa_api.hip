@@ -1,0 +1,226 @@
+// Public C ABI of libsa.so: argument validation, workspace sizing, error
+// reporting, dispatch to the kernel launchers.  Every check runs on the host
+// before any launch, so a rejected call writes nothing.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/sa.h"
+#include "sa_device.h"
+#include "sa_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return SA_OK;
+}
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    return fail(SA_ERR_HIP, "%s: kernel launch failed: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+bool aligned(const void* p, size_t a) {
+  return (reinterpret_cast<uintptr_t>(p) % a) == 0;
+}
+
+// Shared shape checks; returns SA_OK or an error code with the message set.
+int check_common(const char* fn, int B, int H, int L, int d, int dtype, float scale,
+                 int block) {
+  if (B < 1 || H < 1 || L < 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: B=%d H=%d L=%d must all be >= 1", fn, B, H, L);
+  if (dtype != SA_BF16 && dtype != SA_F32)
+    return fail(SA_ERR_UNSUPPORTED, "%s: dtype %d is neither SA_BF16 nor SA_F32", fn, dtype);
+  if (d != 64 && d != 128)
+    return fail(SA_ERR_UNSUPPORTED, "%s: head dim d=%d not in {64, 128}", fn, d);
+  if (block != 64 && block != 128)
+    return fail(SA_ERR_UNSUPPORTED, "%s: block=%d not in {64, 128}", fn, block);
+  const long long n_b = (static_cast<long long>(L) + block - 1) / block;
+  if (n_b > sa::kMaxBlocks)
+    return fail(SA_ERR_UNSUPPORTED, "%s: n_b=%lld blocks exceeds %d", fn, n_b,
+                sa::kMaxBlocks);
+  if (!(scale > 0.f) || !isfinite(scale))
+    return fail(SA_ERR_INVALID_ARG, "%s: scale=%g must be finite and > 0", fn,
+                static_cast<double>(scale));
+  return SA_OK;
+}
+
+int check_tensor(const char* fn, const char* name, const void* p, bool required,
+                 size_t align) {
+  if (p == nullptr) {
+    if (required) return fail(SA_ERR_INVALID_ARG, "%s: %s is NULL", fn, name);
+    return SA_OK;
+  }
+  if (!aligned(p, align))
+    return fail(SA_ERR_INVALID_ARG, "%s: %s is not %zu-byte aligned", fn, name, align);
+  return SA_OK;
+}
+
+int check_ws(const char* fn, const void* ws, size_t ws_bytes, size_t need) {
+  if (ws_bytes < need)
+    return fail(SA_ERR_WORKSPACE, "%s: workspace of %zu bytes is below the %zu required",
+                fn, ws_bytes, need);
+  if (need > 0 && ws == nullptr) return fail(SA_ERR_INVALID_ARG, "%s: ws is NULL", fn);
+  if (need > 0 && !aligned(ws, 16))
+    return fail(SA_ERR_INVALID_ARG, "%s: ws is not 16-byte aligned", fn);
+  return SA_OK;
+}
+
+#define SA_TRY(expr)          \
+  do {                        \
+    const int rc_ = (expr);   \
+    if (rc_ != SA_OK) return rc_; \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int sa_version(void) { return 100; }
+
+const char* sa_last_error(void) { return g_last_error.c_str(); }
+
+size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d, int block) {
+  if (B < 1 || H < 1 || L_v < 1 || (d != 64 && d != 128) || (block != 64 && block != 128))
+    return 0;
+  const int n_b = sa::ceil_div(L_v, block);
+  if (n_b > sa::kMaxBlocks) return 0;
+  switch (call) {
+    case SA_CALL_CROSS_SCORES:
+      if (L_a < 1) return 0;
+      return sa::cross_ws_layout(B, H, L_v, L_a).total;
+    case SA_CALL_BUILD_BLOCK_MASK:
+      return sa::mask_ws_layout(B, H, n_b, d).total;
+    case SA_CALL_SPARSE_ATTENTION:
+      return sa::attn_ws_layout(B, H, n_b, d, block).total;
+    case SA_CALL_SELECT_PROTECTED:
+      return 0;
+    default:
+      return 0;
+  }
+}
+
+int sa_cross_scores(const void* q_a, const void* k_v, const void* q_v, const void* k_a,
+                    int B, int H, int L_v, int L_a, int d, int dtype, float scale,
+                    int block, float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
+                    int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sa_cross_scores";
+  SA_TRY(check_common(fn, B, H, L_v, d, dtype, scale, block));
+  if (L_a < 1) return fail(SA_ERR_INVALID_ARG, "%s: L_a=%d must be >= 1", fn, L_a);
+  if (accumulate != 0 && accumulate != 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: accumulate=%d must be 0 or 1", fn, accumulate);
+  const bool rev = q_v != nullptr;
+  if ((k_a != nullptr) != rev || (sal_a_tok != nullptr) != rev)
+    return fail(SA_ERR_INVALID_ARG,
+                "%s: q_v, k_a and sal_a_tok must be all NULL or all non-NULL", fn);
+  SA_TRY(check_tensor(fn, "q_a", q_a, true, 16));
+  SA_TRY(check_tensor(fn, "k_v", k_v, true, 16));
+  SA_TRY(check_tensor(fn, "q_v", q_v, false, 16));
+  SA_TRY(check_tensor(fn, "k_a", k_a, false, 16));
+  SA_TRY(check_tensor(fn, "sal_v_tok", sal_v_tok, false, 4));
+  SA_TRY(check_tensor(fn, "sal_v_blk", sal_v_blk, true, 4));
+  SA_TRY(check_tensor(fn, "sal_a_tok", sal_a_tok, false, 4));
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::cross_ws_layout(B, H, L_v, L_a).total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  if (dtype == SA_BF16)
+    sa::launch_cross_scores_bf16(
+        static_cast<const uint16_t*>(q_a), static_cast<const uint16_t*>(k_v),
+        static_cast<const uint16_t*>(q_v), static_cast<const uint16_t*>(k_a), B, H, L_v,
+        L_a, d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, w, s);
+  else
+    sa::launch_cross_scores_f32(
+        static_cast<const float*>(q_a), static_cast<const float*>(k_v),
+        static_cast<const float*>(q_v), static_cast<const float*>(k_a), B, H, L_v, L_a,
+        d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, w, s);
+  return check_launch(fn);
+}
+
+int sa_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
+                        int32_t* prot_idx, uint8_t* prot_flag, void* stream) {
+  const char* fn = "sa_select_protected";
+  if (B < 1 || n_b < 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: B=%d n_b=%d must be >= 1", fn, B, n_b);
+  if (n_b > sa::kMaxBlocks)
+    return fail(SA_ERR_UNSUPPORTED, "%s: n_b=%d exceeds %d", fn, n_b, sa::kMaxBlocks);
+  if (k_prot < 0 || k_prot > n_b)
+    return fail(SA_ERR_INVALID_ARG, "%s: k_prot=%d outside [0, n_b=%d]", fn, k_prot, n_b);
+  SA_TRY(check_tensor(fn, "sal_blk", sal_blk, true, 4));
+  SA_TRY(check_tensor(fn, "prot_idx", prot_idx, false, 4));
+  SA_TRY(check_tensor(fn, "prot_flag", prot_flag, true, 1));
+  sa::launch_select_protected(sal_blk, B, n_b, k_prot, prot_idx, prot_flag,
+                              static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_build_block_mask(const void* q_v, const void* k_v, int B, int H, int L_v, int d,
+                        int dtype, float scale, int block, int k_keep,
+                        const uint8_t* prot_flag, int32_t* kv_idx, int32_t* kv_cnt,
+                        uint8_t* mask, float* scores, void* ws, size_t ws_bytes,
+                        void* stream) {
+  const char* fn = "sa_build_block_mask";
+  SA_TRY(check_common(fn, B, H, L_v, d, dtype, scale, block));
+  const int n_b = sa::ceil_div(L_v, block);
+  if (k_keep < 1 || k_keep > n_b)
+    return fail(SA_ERR_INVALID_ARG, "%s: k_keep=%d outside [1, n_b=%d]", fn, k_keep, n_b);
+  SA_TRY(check_tensor(fn, "q_v", q_v, true, 16));
+  SA_TRY(check_tensor(fn, "k_v", k_v, true, 16));
+  SA_TRY(check_tensor(fn, "prot_flag", prot_flag, false, 1));
+  SA_TRY(check_tensor(fn, "kv_idx", kv_idx, true, 4));
+  SA_TRY(check_tensor(fn, "kv_cnt", kv_cnt, true, 4));
+  SA_TRY(check_tensor(fn, "mask", mask, false, 1));
+  SA_TRY(check_tensor(fn, "scores", scores, false, 4));
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::mask_ws_layout(B, H, n_b, d).total));
+  sa::launch_build_block_mask(q_v, k_v, B, H, L_v, d, dtype, scale, block, k_keep,
+                              prot_flag, kv_idx, kv_cnt, mask, scores,
+                              static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_sparse_attention(const void* q, const void* k, const void* v, void* o, float* lse,
+                        int B, int H, int L, int d, int dtype, float scale, int block,
+                        const int32_t* kv_idx, const int32_t* kv_cnt, void* ws,
+                        size_t ws_bytes, void* stream) {
+  const char* fn = "sa_sparse_attention";
+  SA_TRY(check_common(fn, B, H, L, d, dtype, scale, block));
+  SA_TRY(check_tensor(fn, "q", q, true, 16));
+  SA_TRY(check_tensor(fn, "k", k, true, 16));
+  SA_TRY(check_tensor(fn, "v", v, true, 16));
+  SA_TRY(check_tensor(fn, "o", o, true, 16));
+  SA_TRY(check_tensor(fn, "lse", lse, false, 4));
+  SA_TRY(check_tensor(fn, "kv_idx", kv_idx, true, 4));
+  SA_TRY(check_tensor(fn, "kv_cnt", kv_cnt, true, 4));
+  const int n_b = sa::ceil_div(L, block);
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::attn_ws_layout(B, H, n_b, d, block).total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == SA_BF16)
+    sa::launch_sparse_attention_bf16(
+        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+        static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, B, H, L, d,
+        scale, block, kv_idx, kv_cnt, static_cast<char*>(ws), s);
+  else
+    sa::launch_sparse_attention_f32(
+        static_cast<const float*>(q), static_cast<const float*>(k),
+        static_cast<const float*>(v), static_cast<float*>(o), lse, B, H, L, d, scale,
+        block, kv_idx, kv_cnt, static_cast<char*>(ws), s);
+  return check_launch(fn);
+}
+
+}  // extern "C"

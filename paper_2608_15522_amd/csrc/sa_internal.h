@@ -1,0 +1,109 @@
+// Host-side internals of libsa.so: workspace layout and kernel launchers.
+// The public entry points (sa_api.hip) validate every argument, then call
+// these launchers, which only enqueue kernels on the given stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sa {
+
+// Tunables fixed at build time.
+constexpr int kLseChunk = 1024;   // video keys per a->v log-sum-exp partial
+constexpr int kQSlab = 512;       // queries per 16-wave workgroup slab
+constexpr int kHeadGroup = 4;     // heads per a->v column-mass partial
+constexpr int kV2aChunk = 512;    // video queries per v->a workgroup
+constexpr int kMaxBlocks = 2048;  // largest supported n_b
+
+inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Workspace of sa_cross_scores (both dtypes are covered).
+struct CrossWs {
+  size_t lse_part;   // float2 [B,H,nchunk,L_a]  (m, l) partials, bf16 path
+  size_t lse_a;      // float  [B,H,L_a]         a->v log2-sum-exp
+  size_t colmass;    // float  [B,ngroup,L_v]    per head-group column mass
+  size_t lse_v;      // float  [B,H,L_v]         v->a log2-sum-exp, f32 path
+  size_t v2a_part;   // float  [B,H,nchunk3,L_a] v->a column-mass partials
+  size_t total;
+};
+
+inline CrossWs cross_ws_layout(int B, int H, int L_v, int L_a) {
+  CrossWs w{};
+  const size_t nchunk = (L_v + kLseChunk - 1) / kLseChunk;
+  const size_t ngroup = (H + kHeadGroup - 1) / kHeadGroup;
+  const size_t nchunk3 = (L_v + kV2aChunk - 1) / kV2aChunk;
+  size_t off = 0;
+  w.lse_part = off; off += align_up(sizeof(float) * 2 * B * H * nchunk * L_a);
+  w.lse_a = off;    off += align_up(sizeof(float) * B * H * L_a);
+  w.colmass = off;  off += align_up(sizeof(float) * B * ngroup * L_v);
+  w.lse_v = off;    off += align_up(sizeof(float) * B * H * L_v);
+  w.v2a_part = off; off += align_up(sizeof(float) * B * H * nchunk3 * L_a);
+  w.total = off;
+  return w;
+}
+
+struct MaskWs {
+  size_t qbar;   // double [B,H,n_b,d]
+  size_t kbar;   // double [B,H,n_b,d]
+  size_t total;
+};
+
+inline MaskWs mask_ws_layout(int B, int H, int n_b, int d) {
+  MaskWs w{};
+  size_t off = 0;
+  w.qbar = off; off += align_up(sizeof(double) * B * H * n_b * d);
+  w.kbar = off; off += align_up(sizeof(double) * B * H * n_b * d);
+  w.total = off;
+  return w;
+}
+
+struct AttnWs {
+  size_t vt;      // bf16 [B,H,d,n_b*block]  V transposed, zero past L
+  size_t order;   // int  [B,H,n_b]           query blocks, heaviest first
+  size_t total;
+};
+
+inline AttnWs attn_ws_layout(int B, int H, int n_b, int d, int block) {
+  AttnWs w{};
+  size_t off = 0;
+  w.vt = off;    off += align_up(sizeof(uint16_t) * B * H * d * (size_t)n_b * block);
+  w.order = off; off += align_up(sizeof(int32_t) * B * H * n_b);
+  w.total = off;
+  return w;
+}
+
+// ---- launchers (defined in the kernel sources) ----------------------------
+void launch_cross_scores_bf16(const uint16_t* q_a, const uint16_t* k_v,
+                              const uint16_t* q_v, const uint16_t* k_a, int B,
+                              int H, int L_v, int L_a, int d, float scale,
+                              int block, float* sal_v_tok, float* sal_v_blk,
+                              float* sal_a_tok, int accumulate, char* ws,
+                              hipStream_t s);
+void launch_cross_scores_f32(const float* q_a, const float* k_v,
+                             const float* q_v, const float* k_a, int B, int H,
+                             int L_v, int L_a, int d, float scale, int block,
+                             float* sal_v_tok, float* sal_v_blk,
+                             float* sal_a_tok, int accumulate, char* ws,
+                             hipStream_t s);
+void launch_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
+                             int32_t* prot_idx, uint8_t* prot_flag,
+                             hipStream_t s);
+void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
+                             int L_v, int d, int dtype, float scale, int block,
+                             int k_keep, const uint8_t* prot_flag,
+                             int32_t* kv_idx, int32_t* kv_cnt, uint8_t* mask,
+                             float* scores, char* ws, hipStream_t s);
+void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
+                                  const uint16_t* v, uint16_t* o, float* lse,
+                                  int B, int H, int L, int d, float scale,
+                                  int block, const int32_t* kv_idx,
+                                  const int32_t* kv_cnt, char* ws,
+                                  hipStream_t s);
+void launch_sparse_attention_f32(const float* q, const float* k,
+                                 const float* v, float* o, float* lse, int B,
+                                 int H, int L, int d, float scale, int block,
+                                 const int32_t* kv_idx, const int32_t* kv_cnt,
+                                 char* ws, hipStream_t s);
+
+}  // namespace sa

@@ -154,6 +154,8 @@ def _planted_tokens(w: Workload, rng: np.random.Generator) -> np.ndarray:
     if w.plant == "blocks":
         n_full = w.L_v // w.block
         for b in range(w.B):
+            if w.n_plant == 0:
+                continue
             blocks = rng.choice(n_full, w.n_plant, replace=False)
             for c in blocks:
                 mask[b, c * w.block:(c + 1) * w.block] = True

@@ -1,0 +1,138 @@
+"""Host side of the C ABI, on the CPU: the library loads, exports every symbol
+the header declares, sizes workspaces, and rejects bad arguments before any
+launch.  No call here reaches a kernel (every call is invalid)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_15522_amd as sa
+from paper_2608_15522_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sa.h")
+
+FAKE = 0x10000          # aligned stand-in pointer, never dereferenced
+MISALIGNED = 0x10001
+
+pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIB_PATH),
+                                reason="libsa.so not built")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sa_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_symbols()
+    assert set(names) == set(binding.SIGNATURES), names
+    lib = sa.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sa.sa_version() == 100
+
+
+def test_workspace_sizes():
+    for call in (sa.SA_CALL_CROSS_SCORES, sa.SA_CALL_BUILD_BLOCK_MASK,
+                 sa.SA_CALL_SPARSE_ATTENTION):
+        a = sa.sa_workspace_size(call, 1, 24, 32760, 512, 128, 128)
+        b = sa.sa_workspace_size(call, 2, 24, 75600, 1024, 128, 128)
+        assert 0 < a < b
+    # V^T copy: B*H*d*n_b*block bf16 dominates the attention workspace
+    assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, 1, 24, 32760, 512,
+                                128, 128) >= 24 * 128 * 256 * 128 * 2
+    assert sa.sa_workspace_size(sa.SA_CALL_SELECT_PROTECTED, 1, 1, 10, 1, 64, 64) == 0
+    for bad in [(0, 1, 10, 1, 64, 64), (1, 1, 10, 1, 96, 64),
+                (1, 1, 10, 1, 64, 32), (1, 1, 2049 * 128, 1, 64, 128)]:
+        assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, *bad) == 0
+    assert sa.sa_workspace_size(sa.SA_CALL_CROSS_SCORES, 1, 1, 10, 0, 64, 64) == 0
+    assert sa.sa_workspace_size(9, 1, 1, 10, 1, 64, 64) == 0
+
+
+def _attn(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
+             dtype=0, scale=0.088, block=128, kv_idx=FAKE, kv_cnt=FAKE, ws=FAKE,
+             ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return sa.lib().sa_sparse_attention(*a.values())
+
+
+def _mask(**kw):
+    a = dict(q_v=FAKE, k_v=FAKE, B=1, H=1, L_v=1000, d=128, dtype=0, scale=0.088,
+             block=128, k_keep=2, prot_flag=None, kv_idx=FAKE, kv_cnt=FAKE,
+             mask=None, scores=None, ws=FAKE, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return sa.lib().sa_build_block_mask(*a.values())
+
+
+def _cross(**kw):
+    a = dict(q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, B=1, H=1, L_v=1000, L_a=64,
+             d=128, dtype=0, scale=0.088, block=128, sal_v_tok=None,
+             sal_v_blk=FAKE, sal_a_tok=FAKE, accumulate=0, ws=FAKE,
+             ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return sa.lib().sa_cross_scores(*a.values())
+
+
+def _select(**kw):
+    a = dict(sal_blk=FAKE, B=1, n_b=8, k_prot=2, prot_idx=None, prot_flag=FAKE,
+             stream=None)
+    a.update(kw)
+    return sa.lib().sa_select_protected(*a.values())
+
+
+@pytest.mark.parametrize("call,kw,code,needle", [
+    (_attn, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
+    (_attn, dict(block=32), sa.SA_ERR_UNSUPPORTED, "block"),
+    (_attn, dict(dtype=7), sa.SA_ERR_UNSUPPORTED, "dtype"),
+    (_attn, dict(L=2049 * 128), sa.SA_ERR_UNSUPPORTED, "n_b"),
+    (_attn, dict(B=0), sa.SA_ERR_INVALID_ARG, ">= 1"),
+    (_attn, dict(L=0), sa.SA_ERR_INVALID_ARG, ">= 1"),
+    (_attn, dict(scale=0.0), sa.SA_ERR_INVALID_ARG, "scale"),
+    (_attn, dict(scale=float("nan")), sa.SA_ERR_INVALID_ARG, "scale"),
+    (_attn, dict(scale=float("inf")), sa.SA_ERR_INVALID_ARG, "scale"),
+    (_attn, dict(q=None), sa.SA_ERR_INVALID_ARG, "q is NULL"),
+    (_attn, dict(o=None), sa.SA_ERR_INVALID_ARG, "o is NULL"),
+    (_attn, dict(kv_cnt=None), sa.SA_ERR_INVALID_ARG, "kv_cnt is NULL"),
+    (_attn, dict(v=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_attn, dict(lse=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_attn, dict(ws_bytes=16), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_attn, dict(ws=None), sa.SA_ERR_INVALID_ARG, "ws is NULL"),
+    (_mask, dict(k_keep=0), sa.SA_ERR_INVALID_ARG, "k_keep"),
+    (_mask, dict(k_keep=9), sa.SA_ERR_INVALID_ARG, "k_keep"),
+    (_mask, dict(kv_idx=None), sa.SA_ERR_INVALID_ARG, "kv_idx is NULL"),
+    (_mask, dict(scores=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_mask, dict(ws_bytes=0), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_mask, dict(d=32), sa.SA_ERR_UNSUPPORTED, "head dim"),
+    (_cross, dict(L_a=0), sa.SA_ERR_INVALID_ARG, "L_a"),
+    (_cross, dict(accumulate=2), sa.SA_ERR_INVALID_ARG, "accumulate"),
+    (_cross, dict(k_a=None), sa.SA_ERR_INVALID_ARG, "all NULL"),
+    (_cross, dict(sal_a_tok=None), sa.SA_ERR_INVALID_ARG, "all NULL"),
+    (_cross, dict(q_v=None, k_a=None), sa.SA_ERR_INVALID_ARG, "all NULL"),
+    (_cross, dict(sal_v_blk=None), sa.SA_ERR_INVALID_ARG, "sal_v_blk is NULL"),
+    (_cross, dict(q_a=None), sa.SA_ERR_INVALID_ARG, "q_a is NULL"),
+    (_cross, dict(ws_bytes=1), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_select, dict(k_prot=-1), sa.SA_ERR_INVALID_ARG, "k_prot"),
+    (_select, dict(k_prot=9), sa.SA_ERR_INVALID_ARG, "k_prot"),
+    (_select, dict(n_b=0), sa.SA_ERR_INVALID_ARG, "n_b"),
+    (_select, dict(n_b=4096, k_prot=1), sa.SA_ERR_UNSUPPORTED, "n_b"),
+    (_select, dict(prot_flag=None), sa.SA_ERR_INVALID_ARG, "prot_flag is NULL"),
+    (_select, dict(sal_blk=MISALIGNED + 1), sa.SA_ERR_INVALID_ARG, "aligned"),
+])
+def test_invalid_arguments_are_rejected(call, kw, code, needle):
+    rc = call(**kw)
+    assert rc == code
+    msg = sa.sa_last_error()
+    assert needle in msg, msg
+
+
+def test_binding_raises_without_gpu_tensors():
+    import torch
+    x = torch.zeros(1, 1, 128, 64)
+    with pytest.raises(ValueError):
+        sa.sa_sparse_attention(x, x, x, 0.125, 64,
+                               torch.zeros(1, 1, 2, 2, dtype=torch.int32),
+                               torch.zeros(1, 1, 2, dtype=torch.int32), ws=x)
