@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Benchmark of one protected sparse video-attention layer on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input,
+with every input already resident in HBM: cross-modal saliency (both
+directions), protected block selection, the protected pooled-QK block mask
+and block-sparse flash attention -- the four C-ABI calls, on one stream.
+
+Printed (one JSON line): ``value`` = effective dense-equivalent TFLOP/s of
+the layer (4*B*H*L_v^2*d / layer time), ``ms_per_step`` = ms per layer, a
+per-call breakdown from HIP events, the roofline of the dominant kernel
+(block-sparse attention, bf16 MFMA), the speedup over the same kernel run
+with every list full, and the fp64 oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="ovi_bf16")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-heads", type=int, default=3,
+                   help="heads of the layer the oracle is timed on")
+    p.add_argument("--dense-steps", type=int, default=5)
+    p.add_argument("--sweep", default=None,
+                   help="also run the density x protection sweep, one JSON "
+                        "line per cell appended to this file")
+    return p.parse_args()
+
+
+def computed_flops(kv_idx, kv_cnt, L, block, d):
+    """Exact attention flops over the kept (query block, key block) pairs,
+    tails counted at their true length (4 * d per query-key pair)."""
+    import numpy as np
+    B, H, n_b = kv_cnt.shape
+    lens = np.minimum((np.arange(n_b) + 1) * block, L) - np.arange(n_b) * block
+    total = 0
+    for b in range(B):
+        for h in range(H):
+            cnt = kv_cnt[b, h]
+            for r in range(n_b):
+                total += int(lens[r]) * int(lens[kv_idx[b, h, r, :cnt[r]]].sum())
+    return 4 * d * total
+
+
+def time_layer(plan, t, steps, warmup, torch):
+    for _ in range(warmup):
+        plan.run(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        e = ev[i]
+        e[0].record()
+        plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        e[1].record()
+        plan.select_protected()
+        e[2].record()
+        plan.build_block_mask(t["q_v"], t["k_v"])
+        e[3].record()
+        plan.sparse_attention(t["q_v"], t["k_v"], t["v_v"])
+        e[4].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    names = ["sa_cross_scores", "sa_select_protected", "sa_build_block_mask",
+             "sa_sparse_attention"]
+    per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
+                for j, n in enumerate(names)}
+    return wall * 1e3 / steps, per_call
+
+
+def time_attention(plan, t, kv_idx, kv_cnt, steps, torch, sa):
+    sa.sa_sparse_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, plan.block,
+                           kv_idx, kv_cnt, o=plan.o, ws=plan.ws)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        sa.sa_sparse_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, plan.block,
+                               kv_idx, kv_cnt, o=plan.o, ws=plan.ws)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def cpu_baseline(w, x, kv_idx, kv_cnt, heads):
+    """The oracle as it stands, timed on `heads` heads of the layer (every
+    step is per head, so the full-layer time is the sample scaled by H/heads).
+    Returns the dict of the report."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    hs = slice(0, heads)
+    sub = {k: x[k][:, hs] for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
+    t0 = time.perf_counter()
+    oracle.cross_scores(sub["q_a"], sub["k_v"], w.scale, sub["q_v"], sub["k_a"])
+    prot = np.zeros((w.B, w.n_b), dtype=np.uint8)
+    oracle.block_mask(sub["q_v"], sub["k_v"], w.scale, w.block, w.k_keep, prot)
+    oracle.masked_attention(sub["q_v"], sub["k_v"], sub["v_v"], w.scale, w.block,
+                            kv_idx[:, hs], kv_cnt[:, hs])
+    dt = time.perf_counter() - t0
+    layer_s = dt * w.H / heads
+    dense = 4.0 * w.B * w.H * w.L_v ** 2 * w.d
+    return {"value": round(dense / layer_s / 1e12, 6), "unit": "TFLOP/s",
+            "cores": int(cores), "kind": "oracle",
+            "ms_per_layer": round(layer_s * 1e3, 1),
+            "sample": (f"{heads} of {w.H} heads of the {w.name} layer (saliency in "
+                       f"both directions, pooled-QK block mask, sparse attention on "
+                       f"the GPU's lists), {dt:.1f} s, scaled by {w.H}/{heads}")}
+
+
+def run_sweep(path, steps, torch, sa, synth, LayerPlan):
+    """Density x protection sweep at the Ovi-like shape: attention-kernel time
+    of each cell against the same kernel with every list full."""
+    base = synth.WORKLOADS["ovi_bf16"]
+    with open(path, "a") as f:
+        for seed in (0, 1, 2):
+            x = synth.make_inputs(base.with_(seed=seed))
+            t = {k: torch.from_numpy(x[k]).to(torch.bfloat16).cuda()
+                 for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
+            del x
+            dense_ms = None
+            for w in [s for s in synth.sweep_workloads() if s.seed == seed]:
+                plan = LayerPlan(w.B, w.H, w.L_v, w.L_a, w.d, w.block, w.k_keep,
+                                 w.k_prot, w.scale)
+                plan.run(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+                ms = time_attention(plan, t, plan.kv_idx, plan.kv_cnt, steps, torch, sa)
+                if dense_ms is None:
+                    n_b = w.n_b
+                    di = torch.arange(n_b, dtype=torch.int32, device="cuda").expand(
+                        w.B, w.H, n_b, n_b).contiguous()
+                    dc = torch.full((w.B, w.H, n_b), n_b, dtype=torch.int32, device="cuda")
+                    dense_ms = time_attention(plan, t, di, dc, steps, torch, sa)
+                cnt = plan.kv_cnt.cpu().numpy()
+                frac = float(cnt.sum()) / (w.B * w.H * w.n_b * w.n_b)
+                rec = {"cell": w.name, "density": w.density, "rho": w.rho, "seed": seed,
+                       "k_keep": w.k_keep, "k_prot": w.k_prot, "block_fraction": frac,
+                       "attn_ms": ms, "dense_attn_ms": dense_ms,
+                       "speedup_vs_dense": dense_ms / ms, "ideal_1_over_f": 1.0 / frac}
+                f.write(json.dumps(rec) + "\n")
+                f.flush()
+                print(json.dumps(rec), file=sys.stderr, flush=True)
+                del plan
+            del t
+            torch.cuda.empty_cache()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the "
+              "method's path is measured on one GPU's share at full shape.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    import synth
+    import paper_2608_15522_amd as sa
+    from paper_2608_15522_amd.layer import LayerPlan
+
+    w = synth.WORKLOADS[args.workload]
+    print(f"bench: {w.name} B={w.B} H={w.H} L_v={w.L_v} L_a={w.L_a} d={w.d} "
+          f"block={w.block} k_keep={w.k_keep} k_prot={w.k_prot}", file=sys.stderr,
+          flush=True)
+    x = synth.make_inputs(w)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    t = {k: torch.from_numpy(x[k]).to(dt).cuda() for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
+    plan = LayerPlan(w.B, w.H, w.L_v, w.L_a, w.d, w.block, w.k_keep, w.k_prot, w.scale,
+                     dtype=dt)
+    ms_layer, per_call = time_layer(plan, t, args.steps, args.warmup, torch)
+    print(f"bench: layer {ms_layer:.3f} ms {per_call}", file=sys.stderr, flush=True)
+
+    kv_idx = plan.kv_idx.cpu().numpy()
+    kv_cnt = plan.kv_cnt.cpu().numpy()
+    flops_attn = computed_flops(kv_idx, kv_cnt, w.L_v, w.block, w.d)
+    dense_flops = 4.0 * w.B * w.H * w.L_v ** 2 * w.d
+    n_b = w.n_b
+    di = torch.arange(n_b, dtype=torch.int32, device="cuda").expand(w.B, w.H, n_b, n_b).contiguous()
+    dc = torch.full((w.B, w.H, n_b), n_b, dtype=torch.int32, device="cuda")
+    dense_ms = (time_attention(plan, t, di, dc, args.dense_steps, torch, sa)
+                if args.dense_steps > 0 else None)
+    attn_ms = per_call["sa_sparse_attention"]
+    achieved = flops_attn / (attn_ms * 1e-3) / 1e12
+    res = {
+        "metric": "ms/layer + effective TFLOP/s of protected sparse video attention (1 MI355X)",
+        "value": round(dense_flops / (ms_layer * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_layer, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded Gaussian Q/K/V with planted audio-correlated video blocks)",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "L_v": w.L_v, "L_a": w.L_a,
+                   "d": w.d, "block": w.block, "density": w.density, "k_keep": w.k_keep,
+                   "k_prot": w.k_prot, "n_b": n_b},
+        "per_call_ms": {k: round(v, 4) for k, v in per_call.items()},
+        "attention": {
+            "computed_tflop": round(flops_attn / 1e12, 4),
+            "dense_tflop": round(dense_flops / 1e12, 4),
+            "block_fraction": round(float(kv_cnt.sum()) / (w.B * w.H * n_b * n_b), 5),
+            "ms": round(attn_ms, 4),
+            "effective_dense_tflops": round(dense_flops / (attn_ms * 1e-3) / 1e12, 2),
+            "dense_run_ms": round(dense_ms, 4) if dense_ms else None,
+            "speedup_vs_dense_run": round(dense_ms / attn_ms, 3) if dense_ms else None,
+        },
+        "roofline": {"bound": "mfma", "kernel": "sparse_attn_bf16_kernel",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if args.sweep:
+        run_sweep(args.sweep, max(3, args.dense_steps), torch, sa, synth, LayerPlan)
+    if not args.no_cpu_baseline:
+        del t
+        torch.cuda.empty_cache()
+        res["cpu_baseline"] = cpu_baseline(w, x, kv_idx, kv_cnt, min(args.cpu_heads, w.H))
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -5,20 +5,25 @@
 // ------------------------
 // One workgroup per query block (BLOCK rows, BLOCK/32 waves of 32 query rows
 // each).  The workgroup walks its compacted key-block list; every key block
-// is streamed as 64-key tiles through double-buffered LDS (K as [key][d],
-// V as V^T [d][key], both XOR-swizzled so the MFMA operand reads are free of
-// bank conflicts).  Each wave computes S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16, so a lane owns one query column: the row max and
-// row sum of the online softmax are lane-local, plus one exchange with the
-// lane holding the other 16 keys of the same query.  P^T is packed to bf16 in
-// registers and feeds O^T += V^T P^T directly as the B operand.  The scale is
-// folded into exp2.  Keys past L are -inf, rows past L are never written.
+// is streamed as 64-key tiles of K and V ([key][d], 16-byte chunks XOR-
+// swizzled by row) into double-buffered LDS by global_load_lds_dwordx4, so
+// the copy of tile t+1 runs under the math of tile t without staging
+// registers.  Each wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16,
+// so a lane owns one query column: the row max and row sum of the online
+// softmax are lane-local, plus one exchange with the lane holding the other
+// 16 keys of the same query.  P^T is packed to bf16 in registers and feeds
+// O^T += V^T P^T directly as the B operand; the V^T operand is read from the
+// [key][d] tile with ds_read_b64_tr_b16 (a transposing LDS read).  The scale
+// is folded into exp2; the running output is rescaled only when a lane's max
+// grows by more than 2^8.  Keys past L are -inf, rows past L are never
+// written.
 //
-// V^T comes from a transposing copy into the workspace (zero-filled past L);
-// query blocks are launched heaviest list first (protected rows hold the
-// full list), rank-major over (batch, head) pairs, so that when the pair
-// count is a multiple of 8 every pair stays on one XCD and its K/V tiles are
-// shared through that XCD's L2.
+// Query blocks of a (batch, head) pair are launched heaviest list first
+// (protected rows hold the full list).  With a pair count that is a multiple
+// of 8, each XCD takes every 8th pair and works through them one at a time,
+// so a pair's K/V blocks are shared through one XCD's L2 and only 8 pairs'
+// K/V are live in the Infinity Cache; otherwise the launch is rank-major
+// over pairs.
 //
 // f32 path: a plain per-row online softmax with K/V tiles in LDS (used by the
 // small fp32 workloads; fp32 MFMA would not change its role).
@@ -53,67 +58,80 @@ order_rows_kernel(const int32_t* __restrict__ kv_cnt, int32_t* __restrict__ orde
   }
 }
 
-// V [pair][L][D] -> V^T [pair][D][Lp], zero for keys >= L.  Grid (Lp/64, P).
-template <int D>
-__global__ void __launch_bounds__(256)
-transpose_v_kernel(const uint16_t* __restrict__ v, uint16_t* __restrict__ vt,
-                   int L, int Lp) {
-  constexpr int ROW32 = D / 2 + 1;  // padded row, in 32-bit words
-  __shared__ uint32_t tile[kTile * ROW32];
-  const size_t pair = blockIdx.y;
-  const int key0 = blockIdx.x * kTile;
-  const uint16_t* src = v + pair * L * D;
-  for (int q = threadIdx.x; q < kTile * D / 8; q += 256) {
-    const int row = q / (D / 8), cc = q % (D / 8);
-    u32x4 val = {0u, 0u, 0u, 0u};
-    if (key0 + row < L) val = ldg16(src + static_cast<size_t>(key0 + row) * D + cc * 8);
-    uint32_t* dst = tile + row * ROW32 + cc * 4;
-    dst[0] = val.x; dst[1] = val.y; dst[2] = val.z; dst[3] = val.w;
-  }
-  __syncthreads();
-  const uint16_t* t16 = reinterpret_cast<const uint16_t*>(tile);
-  uint16_t* dst = vt + pair * D * Lp;
-  for (int q = threadIdx.x; q < D * (kTile / 8); q += 256) {
-    const int d = q / (kTile / 8), c = q % (kTile / 8);
-    u32x4 out;
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) uint16_t lds_u16_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+// Rescale the running output only when some lane's max has grown by more
+// than 2^8: the stale max keeps every probability below 256, exact after the
+// final division by the row sum taken against the same max.
+constexpr float kRescaleSlack = 8.0f;
+
+// One 64-key tile of K or V, [key][d] bf16 with 16-byte chunk c of row r
+// stored at chunk c ^ (r % (D/8)), copied global -> LDS without registers
+// (global_load_lds_dwordx4: lane l of an instruction fills bytes
+// [16 l, 16 l + 16) of a 1 KB LDS span).  Rows past L read row L-1 (any
+// finite data: those keys get probability 0).
+template <int D, int NW>
+__device__ __forceinline__ void dma_tile(const uint16_t* src, int key0, int L,
+                                         uint16_t* lds, int wave, int lane) {
+  constexpr int CPR = D / 8;
+  constexpr int ROWS_PER_KB = 1024 / (D * 2);
+  constexpr int SPANS = kTile * D * 2 / 1024;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t lo = t16[(8 * c + 2 * j) * (2 * ROW32) + d];
-      const uint32_t hi = t16[(8 * c + 2 * j + 1) * (2 * ROW32) + d];
-      out[j] = lo | (hi << 16);
-    }
-    stg16(dst + static_cast<size_t>(d) * Lp + key0 + 8 * c, out);
+  for (int i = 0; i < SPANS / NW; ++i) {
+    const int span = wave + NW * i;
+    const int row = span * ROWS_PER_KB + lane / CPR;
+    const int phys = lane % CPR;
+    const int chunk = phys ^ (row & (CPR - 1));
+    const int key = min(key0 + row, L - 1);
+    const uint16_t* g = src + static_cast<size_t>(key) * D + chunk * 8;
+    __builtin_amdgcn_global_load_lds(g, (lds_void_t*)(lds + span * 512), 16, 0, 0);
   }
 }
 
+__device__ __forceinline__ void wait_dma() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+}
+
 template <int D, int BLOCK>
-__global__ void __launch_bounds__(BLOCK * 2)
+__global__ void __launch_bounds__(BLOCK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         const uint16_t* __restrict__ k,
-                        const uint16_t* __restrict__ vt,
+                        const uint16_t* __restrict__ v,
                         uint16_t* __restrict__ o, float* __restrict__ lse,
                         const int32_t* __restrict__ kv_idx,
                         const int32_t* __restrict__ kv_cnt,
                         const int32_t* __restrict__ order, int P, int L,
-                        int Lp, int n_b, float c) {
-  constexpr int NT = BLOCK * 2;              // threads per workgroup
-  constexpr int CPR = D / 8;                 // 16-byte chunks per K row
-  constexpr int KCH = kTile * CPR / NT;      // K chunks per thread per tile
-  constexpr int VCH = D * (kTile / 8) / NT;  // V^T chunks per thread per tile
+                        int n_b, float c) {
+  constexpr int NW = BLOCK / 32;             // waves per workgroup
+  constexpr int CPR = D / 8;                 // 16-byte chunks per row
   constexpr int TPB = BLOCK / kTile;         // tiles per key block
   constexpr int KC = D / 16;                 // k-steps of Q K^T
   constexpr int DT = D / 32;                 // 32-row d tiles of O^T
-  static_assert(KCH >= 1 && VCH >= 1, "tile too small for the workgroup");
+  static_assert((kTile * D * 2 / 1024) % NW == 0, "tile spans must split over waves");
 
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTile * D];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][D * kTile];
+  __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][kTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][kTile * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, n = lane & 31;
 
-  const int pair = blockIdx.x % P;
-  const int rank = blockIdx.x / P;
+  // Workgroup w runs on XCD w % 8.  When the pair count is a multiple of 8,
+  // XCD x works through its pairs x, x+8, ... one at a time, heaviest query
+  // block first: the K/V blocks of the pair in flight are shared through that
+  // XCD's L2, and only 8 pairs are live at once across the chip.
+  int pair, rank;
+  if ((P & 7) == 0) {
+    const int i = blockIdx.x >> 3;
+    pair = (blockIdx.x & 7) + 8 * (i / n_b);
+    rank = i % n_b;
+  } else {
+    pair = blockIdx.x % P;
+    rank = blockIdx.x / P;
+  }
   const size_t row_base = static_cast<size_t>(pair) * n_b;
   const int r = order[row_base + rank];
   int cnt = kv_cnt[row_base + r];
@@ -122,7 +140,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 
   const uint16_t* qh = q + static_cast<size_t>(pair) * L * D;
   const uint16_t* kh = k + static_cast<size_t>(pair) * L * D;
-  const uint16_t* vth = vt + static_cast<size_t>(pair) * D * Lp;
+  const uint16_t* vh = v + static_cast<size_t>(pair) * L * D;
 
   const int qrow = r * BLOCK + wave * 32 + n;
   u32x4 qf[KC];
@@ -132,6 +150,13 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                       : u32x4{0u, 0u, 0u, 0u};
   }
 
+  // ds_read_b64_tr_b16 addressing of the PV operand: within each 16-lane
+  // group, source lane i points at V[kb + i/4][db + 4*(i%4) .. +3]; the
+  // instruction then hands lane i the values V[kb + 0..3][db + i].
+  const int grp = lane >> 4, gi = lane & 15;
+  const int tr_key = 4 * (grp >> 1) + (gi >> 2);      // + 16*mm (+ 8)
+  const int tr_d = 16 * (grp & 1) + 4 * (gi & 3);     // + 32*dt
+
   f32x16 acc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
@@ -139,129 +164,101 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   float lsum = 0.f;
 
   const int T = cnt * TPB;
-  u32x4 kr[KCH], vr[VCH];
-
   auto tile_key0 = [&](int t, bool& ok) {
     const int kb = idx[t / TPB];
     const int key0 = kb * BLOCK + kTile * (t % TPB);
     ok = kb >= 0 && kb < n_b && key0 < L;
     return key0;
   };
-  auto load_tile = [&](int t) {
-    bool ok;
-    const int key0 = tile_key0(t, ok);
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int qq = tid + NT * i;
-      const int row = qq / CPR, cc = qq % CPR;
-      kr[i] = (ok && key0 + row < L)
-                  ? ldg16(kh + static_cast<size_t>(key0 + row) * D + cc * 8)
-                  : u32x4{0u, 0u, 0u, 0u};
-    }
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int qq = tid + NT * i;
-      const int d = qq / (kTile / 8), cc = qq % (kTile / 8);
-      vr[i] = ok ? ldg16(vth + static_cast<size_t>(d) * Lp + key0 + cc * 8)
-                 : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int qq = tid + NT * i;
-      const int row = qq / CPR, cc = qq % CPR;
-      stg16(&Ks[buf][row * D + ((cc ^ (row & (CPR - 1))) * 8)], kr[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int qq = tid + NT * i;
-      const int d = qq / (kTile / 8), cc = qq % (kTile / 8);
-      const int s = d & 15;
-      const int unit = (2 * cc) ^ (s & 14);  // 8-byte units, pairs stay aligned
-      u32x4 val = vr[i];
-      if (s & 1) val = u32x4{val.z, val.w, val.x, val.y};
-      stg16(&Vs[buf][d * kTile + unit * 4], val);
-    }
-  };
-
-  if (T > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
-
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < T) load_tile(t + 1);
+  auto issue = [&](int t) {
     bool ok;
     const int key0 = tile_key0(t, ok);
     if (ok) {
-      const uint16_t* Kb = Ks[buf];
-      const uint16_t* Vb = Vs[buf];
-      f32x16 s0 = zero16(), s1 = zero16();
+      dma_tile<D, NW>(kh, key0, L, Ks[t & 1], wave, lane);
+      dma_tile<D, NW>(vh, key0, L, Vs[t & 1], wave, lane);
+    }
+  };
+
+  if (T > 0) issue(0);
+  for (int t = 0; t < T; ++t) {
+    const int buf = t & 1;
+    wait_dma();
+    __syncthreads();
+    if (t + 1 < T) issue(t + 1);
+    bool ok;
+    const int key0 = tile_key0(t, ok);
+    if (!ok) continue;  // uniform: the whole workgroup skips this tile
+    const uint16_t* Kb = Ks[buf];
+    const lds_u16_t* Vb = (const lds_u16_t*)Vs[buf];
+    f32x16 s0 = zero16(), s1 = zero16();
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        const int ch = 2 * kc + g;
-        const u32x4 a0 = *reinterpret_cast<const u32x4*>(
-            Kb + n * D + ((ch ^ (n & (CPR - 1))) * 8));
-        const u32x4 a1 = *reinterpret_cast<const u32x4*>(
-            Kb + (32 + n) * D + ((ch ^ ((32 + n) & (CPR - 1))) * 8));
-        s0 = mfma32x32x16(a0, qf[kc], s0);
-        s1 = mfma32x32x16(a1, qf[kc], s1);
+    for (int kc = 0; kc < KC; ++kc) {
+      const int ch = 2 * kc + g;
+      const u32x4 a0 = *reinterpret_cast<const u32x4*>(
+          Kb + n * D + ((ch ^ (n & (CPR - 1))) * 8));
+      const u32x4 a1 = *reinterpret_cast<const u32x4*>(
+          Kb + (32 + n) * D + ((ch ^ ((32 + n) & (CPR - 1))) * 8));
+      s0 = mfma32x32x16(a0, qf[kc], s0);
+      s1 = mfma32x32x16(a1, qf[kc], s1);
+    }
+    if (key0 + kTile > L) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (key0 + crow(i, g) >= L) s0[i] = -INFINITY;
+        if (key0 + 32 + crow(i, g) >= L) s1[i] = -INFINITY;
       }
-      if (key0 + kTile > L) {
+    }
+    float mx = s0[0];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          if (key0 + crow(i, g) >= L) s0[i] = -INFINITY;
-          if (key0 + 32 + crow(i, g) >= L) s1[i] = -INFINITY;
-        }
-      }
-      float mx = s0[0];
+    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
 #pragma unroll
-      for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-      mx = fmaxf(mx, swap_halves(mx));
-      const float m_new = fmaxf(m, mx * c);
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
+    mx = fmaxf(mx, swap_halves(mx)) * c;
+    if (__any(mx > m + kRescaleSlack)) {
+      const float m_new = fmaxf(m, mx);
       const float alpha = fast_exp2(m - m_new);
       m = m_new;
-      float rs = 0.f;
-      uint32_t pb0[8], pb1[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float p0 = fast_exp2(fmaf(s0[2 * i], c, -m_new));
-        const float p1 = fast_exp2(fmaf(s0[2 * i + 1], c, -m_new));
-        const float p2 = fast_exp2(fmaf(s1[2 * i], c, -m_new));
-        const float p3 = fast_exp2(fmaf(s1[2 * i + 1], c, -m_new));
-        rs += (p0 + p1) + (p2 + p3);
-        pb0[i] = pack_bf16x2(p0, p1);
-        pb1[i] = pack_bf16x2(p2, p3);
-      }
-      lsum = fmaf(lsum, alpha, rs);
+      lsum *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
+    }
+    float rs = 0.f;
+    uint32_t pb0[8], pb1[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float p0 = fast_exp2(fmaf(s0[2 * i], c, -m));
+      const float p1 = fast_exp2(fmaf(s0[2 * i + 1], c, -m));
+      const float p2 = fast_exp2(fmaf(s1[2 * i], c, -m));
+      const float p3 = fast_exp2(fmaf(s1[2 * i + 1], c, -m));
+      rs += (p0 + p1) + (p2 + p3);
+      pb0[i] = pack_bf16x2(p0, p1);
+      pb1[i] = pack_bf16x2(p2, p3);
+    }
+    lsum += rs;
+#pragma unroll
+    for (int mm = 0; mm < 4; ++mm) {
+      const uint32_t* pb = (mm < 2) ? pb0 : pb1;
+      const int h = (mm & 1) * 4;
+      const u32x4 b = {pb[h], pb[h + 1], pb[h + 2], pb[h + 3]};
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const int drow = 32 * dt + n;
-        const int sw = drow & 15;
-        const uint16_t* vrow = Vb + drow * kTile;
-#pragma unroll
-        for (int mm = 0; mm < 4; ++mm) {
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + (((4 * mm + g) ^ sw) * 4));
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + (((4 * mm + 2 + g) ^ sw) * 4));
-          const uint32_t* pb = (mm < 2) ? pb0 : pb1;
-          const int h = (mm & 1) * 4;
-          const u32x4 a = {lo.x, lo.y, hi.x, hi.y};
-          const u32x4 b = {pb[h], pb[h + 1], pb[h + 2], pb[h + 3]};
-          acc[dt] = mfma32x32x16(a, b, acc[dt]);
-        }
+        const int d0 = 32 * dt + tr_d;
+        const int k0 = 16 * mm + tr_key;
+        const int k1 = k0 + 8;
+        const lds_s16x4_t* p0 = (const lds_s16x4_t*)(
+            Vb + k0 * D + (((d0 >> 3) ^ (k0 & (CPR - 1))) << 3) + (d0 & 7));
+        const lds_s16x4_t* p1 = (const lds_s16x4_t*)(
+            Vb + k1 * D + (((d0 >> 3) ^ (k1 & (CPR - 1))) << 3) + (d0 & 7));
+        const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            const_cast<lds_s16x4_t*>(p0)));
+        const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            const_cast<lds_s16x4_t*>(p1)));
+        const u32x4 a = {lo.x, lo.y, hi.x, hi.y};
+        acc[dt] = mfma32x32x16(a, b, acc[dt]);
       }
     }
-    if (t + 1 < T) store_tile(buf ^ 1);
-    __syncthreads();
   }
 
   const float ltot = lsum + swap_halves(lsum);
@@ -368,30 +365,23 @@ void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
                                   hipStream_t s) {
   const int n_b = ceil_div(L, block);
   const int P = B * H;
-  const int Lp = n_b * block;
   const AttnWs lay = attn_ws_layout(B, H, n_b, d, block);
-  uint16_t* vt = reinterpret_cast<uint16_t*>(ws + lay.vt);
   int32_t* order = reinterpret_cast<int32_t*>(ws + lay.order);
   const float c = scale * kLog2e;
-  const dim3 tgrid(Lp / kTile, P);
-  if (d == 128)
-    hipLaunchKernelGGL(transpose_v_kernel<128>, tgrid, dim3(256), 0, s, v, vt, L, Lp);
-  else
-    hipLaunchKernelGGL(transpose_v_kernel<64>, tgrid, dim3(256), 0, s, v, vt, L, Lp);
   hipLaunchKernelGGL(order_rows_kernel, dim3(P), dim3(256), 0, s, kv_cnt, order, n_b);
   const dim3 grid(P * n_b);
   if (d == 128 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 128>), grid, dim3(256), 0, s,
-                       q, k, vt, o, lse, kv_idx, kv_cnt, order, P, L, Lp, n_b, c);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
   else if (d == 128 && block == 64)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 64>), grid, dim3(128), 0, s,
-                       q, k, vt, o, lse, kv_idx, kv_cnt, order, P, L, Lp, n_b, c);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
   else if (d == 64 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 128>), grid, dim3(256), 0, s,
-                       q, k, vt, o, lse, kv_idx, kv_cnt, order, P, L, Lp, n_b, c);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
   else
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 64>), grid, dim3(128), 0, s,
-                       q, k, vt, o, lse, kv_idx, kv_cnt, order, P, L, Lp, n_b, c);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
 }
 
 void launch_sparse_attention_f32(const float* q, const float* k,

@@ -21,7 +21,8 @@
 //                        each video query its log-sum-exp (lane-local), pass 2
 //                        recomputes S and reduces the column mass of every
 //                        64-key audio tile across the workgroup.
-//   K3b v2a_finalize   : fixed-order sum over heads and chunks, / (H*L_v).
+//   K3b v2a_chunk_sum  : fixed-order sum over video chunks per head, then
+//       v2a_finalize   : fixed-order sum over heads, / (H*L_v).
 // fp32 inputs use plain per-thread kernels with the same outputs.
 #include "sa_device.h"
 #include "sa_internal.h"
@@ -409,7 +410,28 @@ a2v_finalize_kernel(const float* __restrict__ colmass, float* __restrict__ sal_v
   }
 }
 
-// sal_a_tok[b][j] = sum over (h, chunk) of part / (H*L_v), fixed order.
+// head_sum[pair][j] = sum over video chunks of part[pair][chunk][j]: grid
+// (ceil(L_a/64), P), 256 threads = 4 chunk phases x 64 audio keys, then a
+// fixed-order sum of the 4 phases.
+__global__ void __launch_bounds__(256)
+v2a_chunk_sum_kernel(const float* __restrict__ part, float* __restrict__ head_sum,
+                     int L_a, int nchunk) {
+  __shared__ float red[4][64];
+  const int j = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int ph = threadIdx.x >> 6;
+  const size_t pair = blockIdx.y;
+  float v = 0.f;
+  if (j < L_a)
+    for (int ch = ph; ch < nchunk; ch += 4)
+      v += part[(pair * nchunk + ch) * L_a + j];
+  red[ph][threadIdx.x & 63] = v;
+  __syncthreads();
+  if (ph == 0 && j < L_a)
+    head_sum[pair * L_a + j] = (red[0][threadIdx.x] + red[1][threadIdx.x]) +
+                               (red[2][threadIdx.x] + red[3][threadIdx.x]);
+}
+
+// sal_a_tok[b][j] = sum over nparts of part / (H*L_v), fixed order.
 __global__ void v2a_finalize_kernel(const float* __restrict__ part,
                                     float* __restrict__ sal_a_tok, int B,
                                     int nparts, int L_a, float inv_norm,
@@ -506,11 +528,14 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
   if (q_v != nullptr) {
     float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
+    float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
     hipLaunchKernelGGL(v2a_colmass_kernel<D>, dim3(nchunk3, P), dim3(1024), 0, s, q_v,
                        k_a, v2a_part, L_v, L_a, nchunk3, c);
+    hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
+                       v2a_part, v2a_head, L_a, nchunk3);
     const size_t na = static_cast<size_t>(B) * L_a;
     hipLaunchKernelGGL(v2a_finalize_kernel, dim3((na + 255) / 256), dim3(256), 0, s,
-                       v2a_part, sal_a_tok, B, H * nchunk3, L_a,
+                       v2a_head, sal_a_tok, B, H, L_a,
                        1.0f / (static_cast<float>(H) * static_cast<float>(L_v)), accumulate);
   }
 }

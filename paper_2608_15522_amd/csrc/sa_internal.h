@@ -25,6 +25,7 @@ struct CrossWs {
   size_t colmass;    // float  [B,ngroup,L_v]    per head-group column mass
   size_t lse_v;      // float  [B,H,L_v]         v->a log2-sum-exp, f32 path
   size_t v2a_part;   // float  [B,H,nchunk3,L_a] v->a column-mass partials
+  size_t v2a_head;   // float  [B,H,L_a]         the same summed over chunks
   size_t total;
 };
 
@@ -39,6 +40,7 @@ inline CrossWs cross_ws_layout(int B, int H, int L_v, int L_a) {
   w.colmass = off;  off += align_up(sizeof(float) * B * ngroup * L_v);
   w.lse_v = off;    off += align_up(sizeof(float) * B * H * L_v);
   w.v2a_part = off; off += align_up(sizeof(float) * B * H * nchunk3 * L_a);
+  w.v2a_head = off; off += align_up(sizeof(float) * B * H * L_a);
   w.total = off;
   return w;
 }
@@ -59,15 +61,13 @@ inline MaskWs mask_ws_layout(int B, int H, int n_b, int d) {
 }
 
 struct AttnWs {
-  size_t vt;      // bf16 [B,H,d,n_b*block]  V transposed, zero past L
-  size_t order;   // int  [B,H,n_b]           query blocks, heaviest first
+  size_t order;   // int [B,H,n_b]  query blocks of each head, heaviest first
   size_t total;
 };
 
-inline AttnWs attn_ws_layout(int B, int H, int n_b, int d, int block) {
+inline AttnWs attn_ws_layout(int B, int H, int n_b, int /*d*/, int /*block*/) {
   AttnWs w{};
   size_t off = 0;
-  w.vt = off;    off += align_up(sizeof(uint16_t) * B * H * d * (size_t)n_b * block);
   w.order = off; off += align_up(sizeof(int32_t) * B * H * n_b);
   w.total = off;
   return w;
