@@ -38,6 +38,9 @@ def parse():
     p.add_argument("--cpu-heads", type=int, default=3,
                    help="heads of the layer the oracle is timed on")
     p.add_argument("--dense-steps", type=int, default=5)
+    p.add_argument("--calibrate-copy-mib", type=int, default=0,
+                   help="run one device-to-device copy of this many MiB before "
+                        "timing (a known-size reference for HBM byte counters)")
     p.add_argument("--sweep", default=None,
                    help="also run the density x protection sweep, one JSON "
                         "line per cell appended to this file")
@@ -188,6 +191,14 @@ def main():
     t = {k: torch.from_numpy(x[k]).to(dt).cuda() for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
     plan = LayerPlan(w.B, w.H, w.L_v, w.L_a, w.d, w.block, w.k_keep, w.k_prot, w.scale,
                      dtype=dt)
+    if args.calibrate_copy_mib > 0:
+        nbytes = args.calibrate_copy_mib << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     ms_layer, per_call = time_layer(plan, t, args.steps, args.warmup, torch)
     print(f"bench: layer {ms_layer:.3f} ms {per_call}", file=sys.stderr, flush=True)
 

@@ -5,17 +5,18 @@
 // ------------------------
 // One workgroup per query block (BLOCK rows, BLOCK/32 waves of 32 query rows
 // each).  The workgroup walks its compacted key-block list; every key block
-// is streamed as 64-key tiles of K and V ([key][d], 16-byte chunks XOR-
-// swizzled by row) into double-buffered LDS by global_load_lds_dwordx4, so
-// the copy of tile t+1 runs under the math of tile t without staging
-// registers.  Each wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16,
+// is streamed as 64-key tiles of K and V into double-buffered LDS by
+// global_load_lds_dwordx4 (planes of 32 d per key, 16-byte slots swizzled by
+// row), so the copy of tile t+1 runs under the math of tile t without
+// staging registers.  Each wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16,
 // so a lane owns one query column: the row max and row sum of the online
 // softmax are lane-local, plus one exchange with the lane holding the other
 // 16 keys of the same query.  P^T is packed to bf16 in registers and feeds
 // O^T += V^T P^T directly as the B operand; the V^T operand is read from the
-// [key][d] tile with ds_read_b64_tr_b16 (a transposing LDS read).  The scale
-// is folded into exp2; the running output is rescaled only when a lane's max
-// grows by more than 2^8.  Keys past L are -inf, rows past L are never
+// key-major tile with ds_read_b64_tr_b16 (a transposing LDS read).  The row
+// sum is taken on the same bf16 probabilities with v_dot2_f32_bf16.  The
+// scale is folded into exp2; the running output is rescaled only when a
+// lane's max grows by more than 2^8.  Keys past L are -inf, rows past L are never
 // written.
 //
 // Query blocks of a (batch, head) pair are launched heaviest list first
@@ -68,31 +69,54 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 // final division by the row sum taken against the same max.
 constexpr float kRescaleSlack = 8.0f;
 
-// One 64-key tile of K or V, [key][d] bf16 with 16-byte chunk c of row r
-// stored at chunk c ^ (r % (D/8)), copied global -> LDS without registers
-// (global_load_lds_dwordx4: lane l of an instruction fills bytes
-// [16 l, 16 l + 16) of a 1 KB LDS span).  Rows past L read row L-1 (any
-// finite data: those keys get probability 0).
+// LDS tile layout: D/32 "planes" of [64 keys][32 d] bf16 (64 bytes per key
+// row, 4 KB per plane); 16-byte slot s of row r is stored at slot
+// s ^ plane_swz(r).  With this swizzle both the K operand reads
+// (ds_read_b128: 16 consecutive rows, one slot) and the transposing V reads
+// (ds_read_b64_tr_b16: 4 consecutive rows, two slots) are free of bank
+// conflicts, and every read address is a lane constant plus an immediate.
+__device__ __forceinline__ constexpr int plane_swz(int r) {
+  return ((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1);
+}
+
+// Byte offset, inside a tile, of 16-byte DMA chunk i (0 .. 4*D-1): the LDS
+// byte 16*i belongs to plane i/256, row (i%256)/4, physical slot i%4.  The
+// return value is the global byte offset, relative to the tile's first key
+// row, of the data that belongs there.
+template <int D>
+__device__ __forceinline__ uint32_t dma_src_offset(int i, int key_row_limit) {
+  const int plane = i >> 8;
+  const int row = (i >> 2) & 63;
+  const int logical = (i & 3) ^ plane_swz(row);
+  const int r = row < key_row_limit ? row : key_row_limit;
+  return static_cast<uint32_t>(r * D * 2 + plane * 64 + logical * 16);
+}
+
+// Copy one 64-key tile (rows key0 .. key0+63 of a [L][D] bf16 matrix)
+// global -> LDS with global_load_lds_dwordx4: instruction i of wave w fills
+// the 1 KB span (w + NW*i) of the tile, lane l its 16 bytes at 16*l.
 template <int D, int NW>
-__device__ __forceinline__ void dma_tile(const uint16_t* src, int key0, int L,
-                                         uint16_t* lds, int wave, int lane) {
-  constexpr int CPR = D / 8;
-  constexpr int ROWS_PER_KB = 1024 / (D * 2);
+__device__ __forceinline__ void dma_tile(const char* tile_src, const uint32_t* src_off,
+                                         uint16_t* lds, int wave_u) {
   constexpr int SPANS = kTile * D * 2 / 1024;
 #pragma unroll
   for (int i = 0; i < SPANS / NW; ++i) {
-    const int span = wave + NW * i;
-    const int row = span * ROWS_PER_KB + lane / CPR;
-    const int phys = lane % CPR;
-    const int chunk = phys ^ (row & (CPR - 1));
-    const int key = min(key0 + row, L - 1);
-    const uint16_t* g = src + static_cast<size_t>(key) * D + chunk * 8;
-    __builtin_amdgcn_global_load_lds(g, (lds_void_t*)(lds + span * 512), 16, 0, 0);
+    const int span = wave_u + NW * i;
+    __builtin_amdgcn_global_load_lds(tile_src + src_off[i],
+                                     (lds_void_t*)(lds + span * 512), 16, 0, 0);
   }
 }
 
 __device__ __forceinline__ void wait_dma() {
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+}
+
+// Max of x over the two lanes n and n+32 (robust to which half each output
+// of the swap carries).
+__device__ __forceinline__ float max_halves(float x) {
+  const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                   false, false);
+  return fmaxf(x, fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1])));
 }
 
 template <int D, int BLOCK>
@@ -106,17 +130,20 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         const int32_t* __restrict__ order, int P, int L,
                         int n_b, float c) {
   constexpr int NW = BLOCK / 32;             // waves per workgroup
-  constexpr int CPR = D / 8;                 // 16-byte chunks per row
   constexpr int TPB = BLOCK / kTile;         // tiles per key block
   constexpr int KC = D / 16;                 // k-steps of Q K^T
-  constexpr int DT = D / 32;                 // 32-row d tiles of O^T
-  static_assert((kTile * D * 2 / 1024) % NW == 0, "tile spans must split over waves");
+  constexpr int DT = D / 32;                 // 32-row d tiles of O^T (= planes)
+  constexpr int SPANS = kTile * D * 2 / 1024;
+  constexpr int NI = SPANS / NW;             // DMA instructions per wave per matrix
+  constexpr int TILE_ELEMS = kTile * D;
+  static_assert(SPANS % NW == 0, "tile spans must split over waves");
 
-  __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][kTile * D];
-  __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][kTile * D];
+  __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][TILE_ELEMS];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, n = lane & 31;
 
   // Workgroup w runs on XCD w % 8.  When the pair count is a multiple of 8,
@@ -139,10 +166,10 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   const int32_t* idx = kv_idx + (row_base + r) * n_b;
 
   const uint16_t* qh = q + static_cast<size_t>(pair) * L * D;
-  const uint16_t* kh = k + static_cast<size_t>(pair) * L * D;
-  const uint16_t* vh = v + static_cast<size_t>(pair) * L * D;
+  const char* kh = reinterpret_cast<const char*>(k + static_cast<size_t>(pair) * L * D);
+  const char* vh = reinterpret_cast<const char*>(v + static_cast<size_t>(pair) * L * D);
 
-  const int qrow = r * BLOCK + wave * 32 + n;
+  const int qrow = r * BLOCK + (tid >> 6) * 32 + n;
   u32x4 qf[KC];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
@@ -150,12 +177,25 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                       : u32x4{0u, 0u, 0u, 0u};
   }
 
-  // ds_read_b64_tr_b16 addressing of the PV operand: within each 16-lane
-  // group, source lane i points at V[kb + i/4][db + 4*(i%4) .. +3]; the
-  // instruction then hands lane i the values V[kb + 0..3][db + i].
+  // Per-lane DMA source offsets of a full tile (rows past L are clamped in
+  // the tail tile only).
+  uint32_t src_full[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) src_full[i] = dma_src_offset<D>((wave_u + NW * i) * 64 + lane, 63);
+
+  // Lane-constant LDS byte offsets of the operand reads.
+  //  K (A operand of S^T = K Q^T): row 32*st + n, slot 2*(kc&1) + g of plane kc/2.
+  const int k_off0 = n * 64 + 16 * ((0 + g) ^ plane_swz(n));
+  const int k_off1 = n * 64 + 16 * ((2 + g) ^ plane_swz(n));
+  //  V (ds_read_b64_tr_b16): within each 16-lane group, source lane i points
+  //  at V[kb + i/4][db + 4*(i%4) .. +3] so that lane i receives
+  //  V[kb + 0..3][db + i]; rows 16*mm + 8*h + tr_key, d = 32*dt + tr_d.
   const int grp = lane >> 4, gi = lane & 15;
-  const int tr_key = 4 * (grp >> 1) + (gi >> 2);      // + 16*mm (+ 8)
-  const int tr_d = 16 * (grp & 1) + 4 * (gi & 3);     // + 32*dt
+  const int tr_key = 4 * (grp >> 1) + (gi >> 2);
+  const int tr_byte = 32 * (grp & 1) + 8 * (gi & 3);
+  const int v_off0 = tr_key * 64 + 16 * ((tr_byte >> 4) ^ plane_swz(tr_key)) + (tr_byte & 15);
+  const int v_off1 = (8 + tr_key) * 64 + 16 * ((tr_byte >> 4) ^ plane_swz(8 + tr_key)) +
+                     (tr_byte & 15);
 
   f32x16 acc[DT];
 #pragma unroll
@@ -173,11 +213,23 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   auto issue = [&](int t) {
     bool ok;
     const int key0 = tile_key0(t, ok);
-    if (ok) {
-      dma_tile<D, NW>(kh, key0, L, Ks[t & 1], wave, lane);
-      dma_tile<D, NW>(vh, key0, L, Vs[t & 1], wave, lane);
+    if (!ok) return;
+    const size_t base = static_cast<size_t>(key0) * D * 2;
+    if (key0 + kTile <= L) {
+      dma_tile<D, NW>(kh + base, src_full, Ks[t & 1], wave_u);
+      dma_tile<D, NW>(vh + base, src_full, Vs[t & 1], wave_u);
+    } else {
+      uint32_t src_tail[NI];
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        src_tail[i] = dma_src_offset<D>((wave_u + NW * i) * 64 + lane, L - 1 - key0);
+      dma_tile<D, NW>(kh + base, src_tail, Ks[t & 1], wave_u);
+      dma_tile<D, NW>(vh + base, src_tail, Vs[t & 1], wave_u);
     }
   };
+
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
   if (T > 0) issue(0);
   for (int t = 0; t < T; ++t) {
@@ -188,16 +240,14 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     bool ok;
     const int key0 = tile_key0(t, ok);
     if (!ok) continue;  // uniform: the whole workgroup skips this tile
-    const uint16_t* Kb = Ks[buf];
+    const char* Kb = reinterpret_cast<const char*>(Ks[buf]);
     const lds_u16_t* Vb = (const lds_u16_t*)Vs[buf];
     f32x16 s0 = zero16(), s1 = zero16();
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
-      const int ch = 2 * kc + g;
-      const u32x4 a0 = *reinterpret_cast<const u32x4*>(
-          Kb + n * D + ((ch ^ (n & (CPR - 1))) * 8));
-      const u32x4 a1 = *reinterpret_cast<const u32x4*>(
-          Kb + (32 + n) * D + ((ch ^ ((32 + n) & (CPR - 1))) * 8));
+      const int off = (kc & 1) ? k_off1 : k_off0;
+      const u32x4 a0 = *reinterpret_cast<const u32x4*>(Kb + (kc >> 1) * 4096 + off);
+      const u32x4 a1 = *reinterpret_cast<const u32x4*>(Kb + (kc >> 1) * 4096 + 2048 + off);
       s0 = mfma32x32x16(a0, qf[kc], s0);
       s1 = mfma32x32x16(a1, qf[kc], s1);
     }
@@ -213,7 +263,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
 #pragma unroll
     for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-    mx = fmaxf(mx, swap_halves(mx)) * c;
+    mx = max_halves(mx) * c;
     if (__any(mx > m + kRescaleSlack)) {
       const float m_new = fmaxf(m, mx);
       const float alpha = fast_exp2(m - m_new);
@@ -224,19 +274,22 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
     }
-    float rs = 0.f;
     uint32_t pb0[8], pb1[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const float p0 = fast_exp2(fmaf(s0[2 * i], c, -m));
-      const float p1 = fast_exp2(fmaf(s0[2 * i + 1], c, -m));
-      const float p2 = fast_exp2(fmaf(s1[2 * i], c, -m));
-      const float p3 = fast_exp2(fmaf(s1[2 * i + 1], c, -m));
-      rs += (p0 + p1) + (p2 + p3);
-      pb0[i] = pack_bf16x2(p0, p1);
-      pb1[i] = pack_bf16x2(p2, p3);
+      pb0[i] = pack_bf16x2(fast_exp2(fmaf(s0[2 * i], c, -m)),
+                           fast_exp2(fmaf(s0[2 * i + 1], c, -m)));
+      pb1[i] = pack_bf16x2(fast_exp2(fmaf(s1[2 * i], c, -m)),
+                           fast_exp2(fmaf(s1[2 * i + 1], c, -m)));
     }
-    lsum += rs;
+    // row sum of the bf16 probabilities that the PV product uses
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb0[i]), ones,
+                                             lsum, false);
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb1[i]), ones,
+                                             lsum, false);
+    }
 #pragma unroll
     for (int mm = 0; mm < 4; ++mm) {
       const uint32_t* pb = (mm < 2) ? pb0 : pb1;
@@ -244,17 +297,11 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       const u32x4 b = {pb[h], pb[h + 1], pb[h + 2], pb[h + 3]};
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const int d0 = 32 * dt + tr_d;
-        const int k0 = 16 * mm + tr_key;
-        const int k1 = k0 + 8;
-        const lds_s16x4_t* p0 = (const lds_s16x4_t*)(
-            Vb + k0 * D + (((d0 >> 3) ^ (k0 & (CPR - 1))) << 3) + (d0 & 7));
-        const lds_s16x4_t* p1 = (const lds_s16x4_t*)(
-            Vb + k1 * D + (((d0 >> 3) ^ (k1 & (CPR - 1))) << 3) + (d0 & 7));
+        const lds_u16_t* base = Vb + (dt * 4096 + mm * 1024) / 2;
         const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            const_cast<lds_s16x4_t*>(p0)));
+            (lds_s16x4_t*)(base + v_off0 / 2)));
         const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            const_cast<lds_s16x4_t*>(p1)));
+            (lds_s16x4_t*)(base + v_off1 / 2)));
         const u32x4 a = {lo.x, lo.y, hi.x, hi.y};
         acc[dt] = mfma32x32x16(a, b, acc[dt]);
       }

@@ -13,7 +13,8 @@ import paper_2608_15522_amd as sa
 
 TIE = 1e-6          # scores within this of the k-th value may go either way
 TOL_O = {"f32": 1e-5, "bf16": 1.5e-2}
-TOL_LSE = {"f32": 1e-5, "bf16": 1e-3}
+TOL_LSE = {"f32": 1e-5, "bf16": 2.5e-3}   # bf16: the row sum adds the bf16-rounded
+                                             # probabilities (<= 2^-9 relative each)
 TOL_SAL = 1e-6      # on L1-normalised saliency (diagnostic bound)
 
 
