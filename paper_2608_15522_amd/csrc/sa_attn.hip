@@ -95,15 +95,33 @@ __device__ __forceinline__ uint32_t dma_src_offset(int i, int key_row_limit) {
 // Copy one 64-key tile (rows key0 .. key0+63 of a [L][D] bf16 matrix)
 // global -> LDS with global_load_lds_dwordx4: instruction i of wave w fills
 // the 1 KB span (w + NW*i) of the tile, lane l its 16 bytes at 16*l.
+//
+// The copy is issued with inline assembly on purpose: the compiler cannot
+// tell that an in-flight copy into one buffer does not alias the operand
+// reads of the other, and would otherwise wait for every copy (vmcnt(0))
+// before the first LDS read that follows it, serialising the pipeline.  The
+// kernel orders the buffers itself: s_waitcnt vmcnt(0) and a barrier end
+// every iteration, before any copied tile is read or a buffer is refilled.
+__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(gptr), "s"(lds_addr)
+      : "memory", "m0");
+}
+
 template <int D, int NW>
 __device__ __forceinline__ void dma_tile(const char* tile_src, const uint32_t* src_off,
                                          uint16_t* lds, int wave_u) {
   constexpr int SPANS = kTile * D * 2 / 1024;
+  const uint32_t lds_base = (uint32_t)(size_t)(lds_void_t*)lds;  // LDS byte address
 #pragma unroll
   for (int i = 0; i < SPANS / NW; ++i) {
     const int span = wave_u + NW * i;
-    __builtin_amdgcn_global_load_lds(tile_src + src_off[i],
-                                     (lds_void_t*)(lds + span * 512), 16, 0, 0);
+    lds_dma16(tile_src + src_off[i],
+              __builtin_amdgcn_readfirstlane(lds_base + span * 1024));
   }
 }
 
@@ -140,6 +158,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 
   __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][TILE_ELEMS];
   __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][TILE_ELEMS];
+  __shared__ uint16_t tiles[kMaxBlocks * TPB];  // valid tiles, as key0 / 64
+  __shared__ int ntiles_sh;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -164,6 +184,25 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   int cnt = kv_cnt[row_base + r];
   cnt = cnt < 0 ? 0 : (cnt > n_b ? n_b : cnt);
   const int32_t* idx = kv_idx + (row_base + r) * n_b;
+
+  // Compact the list into 64-key tiles (wave 0): entries outside [0, n_b)
+  // are dropped, and so is the second half of a last block of <= 64 keys.
+  if (tid < 64) {
+    int base = 0;
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int i0 = 0; i0 < cnt; i0 += 64) {
+      const int i = i0 + lane;
+      const int kb = i < cnt ? idx[i] : -1;
+      const bool v0 = kb >= 0 && kb < n_b;
+      const bool v1 = TPB == 2 && v0 && kb * BLOCK + kTile < L;
+      const uint64_t b0 = __ballot(v0), b1 = __ballot(v1);
+      const int pos = base + __popcll(b0 & below) + __popcll(b1 & below);
+      if (v0) tiles[pos] = static_cast<uint16_t>(kb * TPB);
+      if (v1) tiles[pos + 1] = static_cast<uint16_t>(kb * TPB + 1);
+      base += __popcll(b0) + __popcll(b1);
+    }
+    if (lane == 0) ntiles_sh = base;
+  }
 
   const uint16_t* qh = q + static_cast<size_t>(pair) * L * D;
   const char* kh = reinterpret_cast<const char*>(k + static_cast<size_t>(pair) * L * D);
@@ -197,52 +236,29 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   const int v_off1 = (8 + tr_key) * 64 + 16 * ((tr_byte >> 4) ^ plane_swz(8 + tr_key)) +
                      (tr_byte & 15);
 
-  f32x16 acc[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
-  float m = -INFINITY;
-  float lsum = 0.f;
-
-  const int T = cnt * TPB;
-  auto tile_key0 = [&](int t, bool& ok) {
-    const int kb = idx[t / TPB];
-    const int key0 = kb * BLOCK + kTile * (t % TPB);
-    ok = kb >= 0 && kb < n_b && key0 < L;
-    return key0;
+  __syncthreads();  // the tile list is visible
+  const int T = ntiles_sh;
+  auto tile_key0 = [&](int t) {
+    return __builtin_amdgcn_readfirstlane(static_cast<int>(tiles[t]) * kTile);
   };
-  auto issue = [&](int t) {
-    bool ok;
-    const int key0 = tile_key0(t, ok);
-    if (!ok) return;
-    const size_t base = static_cast<size_t>(key0) * D * 2;
+  auto issue = [&](const char* src, int t, uint16_t* lds) {
+    const int key0 = tile_key0(t);
+    const char* base = src + static_cast<size_t>(key0) * D * 2;
     if (key0 + kTile <= L) {
-      dma_tile<D, NW>(kh + base, src_full, Ks[t & 1], wave_u);
-      dma_tile<D, NW>(vh + base, src_full, Vs[t & 1], wave_u);
+      dma_tile<D, NW>(base, src_full, lds, wave_u);
     } else {
       uint32_t src_tail[NI];
 #pragma unroll
       for (int i = 0; i < NI; ++i)
         src_tail[i] = dma_src_offset<D>((wave_u + NW * i) * 64 + lane, L - 1 - key0);
-      dma_tile<D, NW>(kh + base, src_tail, Ks[t & 1], wave_u);
-      dma_tile<D, NW>(vh + base, src_tail, Vs[t & 1], wave_u);
+      dma_tile<D, NW>(base, src_tail, lds, wave_u);
     }
   };
-
-  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-  const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-
-  if (T > 0) issue(0);
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    wait_dma();
-    __syncthreads();
-    if (t + 1 < T) issue(t + 1);
-    bool ok;
-    const int key0 = tile_key0(t, ok);
-    if (!ok) continue;  // uniform: the whole workgroup skips this tile
-    const char* Kb = reinterpret_cast<const char*>(Ks[buf]);
-    const lds_u16_t* Vb = (const lds_u16_t*)Vs[buf];
-    f32x16 s0 = zero16(), s1 = zero16();
+  // S^T of one tile: rows 0..31 in s0, 32..63 in s1.
+  auto qk = [&](const uint16_t* Kt, f32x16& s0, f32x16& s1) {
+    const char* Kb = reinterpret_cast<const char*>(Kt);
+    s0 = zero16();
+    s1 = zero16();
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       const int off = (kc & 1) ? k_off1 : k_off0;
@@ -251,6 +267,9 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       s0 = mfma32x32x16(a0, qf[kc], s0);
       s1 = mfma32x32x16(a1, qf[kc], s1);
     }
+  };
+  // Keys past L get -inf, then the lane-local row max.
+  auto mask_and_max = [&](f32x16& s0, f32x16& s1, int key0) {
     if (key0 + kTile > L) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -263,7 +282,36 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
 #pragma unroll
     for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-    mx = max_halves(mx) * c;
+    return mx;
+  };
+
+  f32x16 acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
+  float m = -INFINITY;
+  float lsum = 0.f;
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+
+  // Pipeline: K runs one tile ahead of V.  On entry to iteration t, K(t+1)
+  // and V(t) are in LDS and S(t) is in registers.
+  f32x16 sc0 = zero16(), sc1 = zero16();
+  float mx_cur = -INFINITY;
+  if (T > 0) {
+    issue(kh, 0, Ks[0]);
+    issue(vh, 0, Vs[0]);
+  }
+  if (T > 1) issue(kh, 1, Ks[1]);
+  wait_dma();
+  __syncthreads();
+  if (T > 0) {
+    qk(Ks[0], sc0, sc1);
+    mx_cur = mask_and_max(sc0, sc1, tile_key0(0));
+  }
+  for (int t = 0; t < T; ++t) {
+    if (t + 2 < T) issue(kh, t + 2, Ks[t & 1]);
+    if (t + 1 < T) issue(vh, t + 1, Vs[(t + 1) & 1]);
+    const float mx = max_halves(mx_cur) * c;
     if (__any(mx > m + kRescaleSlack)) {
       const float m_new = fmaxf(m, mx);
       const float alpha = fast_exp2(m - m_new);
@@ -274,13 +322,17 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
     }
+    // S(t+1) on the matrix cores (computed on stale data in the last
+    // iteration and discarded) while the VALUs form P(t).
+    f32x16 sn0, sn1;
+    qk(Ks[(t + 1) & 1], sn0, sn1);
     uint32_t pb0[8], pb1[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      pb0[i] = pack_bf16x2(fast_exp2(fmaf(s0[2 * i], c, -m)),
-                           fast_exp2(fmaf(s0[2 * i + 1], c, -m)));
-      pb1[i] = pack_bf16x2(fast_exp2(fmaf(s1[2 * i], c, -m)),
-                           fast_exp2(fmaf(s1[2 * i + 1], c, -m)));
+      pb0[i] = pack_bf16x2(fast_exp2(fmaf(sc0[2 * i], c, -m)),
+                           fast_exp2(fmaf(sc0[2 * i + 1], c, -m)));
+      pb1[i] = pack_bf16x2(fast_exp2(fmaf(sc1[2 * i], c, -m)),
+                           fast_exp2(fmaf(sc1[2 * i + 1], c, -m)));
     }
     // row sum of the bf16 probabilities that the PV product uses
 #pragma unroll
@@ -290,6 +342,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb1[i]), ones,
                                              lsum, false);
     }
+    // O^T += V(t)^T P(t)^T while the row max of S(t+1) is taken.
+    const lds_u16_t* Vb = (const lds_u16_t*)Vs[t & 1];
 #pragma unroll
     for (int mm = 0; mm < 4; ++mm) {
       const uint32_t* pb = (mm < 2) ? pb0 : pb1;
@@ -306,6 +360,11 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
         acc[dt] = mfma32x32x16(a, b, acc[dt]);
       }
     }
+    if (t + 1 < T) mx_cur = mask_and_max(sn0, sn1, tile_key0(t + 1));
+    sc0 = sn0;
+    sc1 = sn1;
+    wait_dma();
+    __syncthreads();
   }
 
   const float ltot = lsum + swap_halves(lsum);
