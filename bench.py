@@ -26,6 +26,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+ATTN_KERNEL = "sparse_attn_bf16_kernel<128,128>"
+ATTN_SOURCES = ("paper_2608_15522_amd/csrc/sa_attn.hip",
+                "paper_2608_15522_amd/csrc/sa_device.h")
+TRAFFIC_FILE = "profiles/ovi_layer_hbm_bytes.md"
 
 
 def parse():
@@ -45,6 +49,31 @@ def parse():
                    help="also run the density x protection sweep, one JSON "
                         "line per cell appended to this file")
     return p.parse_args()
+
+
+def attention_traffic(workload):
+    """Bytes past L2 per attention launch (FETCH_SIZE + WRITE_SIZE, each scaled
+    by a same-run copy of known size) from the committed counter summary, or
+    None when that summary was taken on another workload or on kernel sources
+    other than the ones in this tree."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    src = h.hexdigest()[:16]
+    try:
+        text = open(os.path.join(ROOT, TRAFFIC_FILE)).read()
+    except OSError:
+        return None, None
+    for line in text.splitlines():
+        if not line.startswith("traffic "):
+            continue
+        kv = dict(f.split("=", 1) for f in line.split()[1:])
+        if (kv.get("kernel") == ATTN_KERNEL and kv.get("workload") == workload
+                and kv.get("src") == src):
+            return int(kv["fetch_bytes"]) + int(kv["write_bytes"]), TRAFFIC_FILE
+    return None, None
 
 
 def computed_flops(kv_idx, kv_cnt, L, block, d):
@@ -213,6 +242,7 @@ def main():
                 if args.dense_steps > 0 else None)
     attn_ms = per_call["sa_sparse_attention"]
     achieved = flops_attn / (attn_ms * 1e-3) / 1e12
+    traffic, traffic_src = attention_traffic(w.name)
     res = {
         "metric": "ms/layer + effective TFLOP/s of protected sparse video attention (1 MI355X)",
         "value": round(dense_flops / (ms_layer * 1e-3) / 1e12, 3),
@@ -235,10 +265,12 @@ def main():
             "dense_run_ms": round(dense_ms, 4) if dense_ms else None,
             "speedup_vs_dense_run": round(dense_ms / attn_ms, 3) if dense_ms else None,
         },
-        "roofline": {"bound": "mfma", "kernel": "sparse_attn_bf16_kernel",
+        "roofline": {"bound": "mfma", "kernel": ATTN_KERNEL,
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": traffic, "traffic_unit": "bytes/launch",
+                     "traffic_src": traffic_src,
+                     "algorithmic_bytes": 4 * w.B * w.H * w.L_v * w.d * (2 if w.dtype == "bf16" else 4)},
     }
     if args.sweep:
         run_sweep(args.sweep, max(3, args.dense_steps), torch, sa, synth, LayerPlan)
