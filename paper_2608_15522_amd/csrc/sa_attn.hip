@@ -79,22 +79,11 @@ __device__ __forceinline__ constexpr int plane_swz(int r) {
   return ((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1);
 }
 
-// Byte offset, inside a tile, of 16-byte DMA chunk i (0 .. 4*D-1): the LDS
-// byte 16*i belongs to plane i/256, row (i%256)/4, physical slot i%4.  The
-// return value is the global byte offset, relative to the tile's first key
-// row, of the data that belongs there.
-template <int D>
-__device__ __forceinline__ uint32_t dma_src_offset(int i, int key_row_limit) {
-  const int plane = i >> 8;
-  const int row = (i >> 2) & 63;
-  const int logical = (i & 3) ^ plane_swz(row);
-  const int r = row < key_row_limit ? row : key_row_limit;
-  return static_cast<uint32_t>(r * D * 2 + plane * 64 + logical * 16);
-}
-
-// Copy one 64-key tile (rows key0 .. key0+63 of a [L][D] bf16 matrix)
-// global -> LDS with global_load_lds_dwordx4: instruction i of wave w fills
-// the 1 KB span (w + NW*i) of the tile, lane l its 16 bytes at 16*l.
+// Copy of 16 bytes per lane, global -> LDS (global_load_lds_dwordx4): lane l
+// writes LDS bytes [lds_addr + 16*l, +16) with the 16 bytes at sbase + voff.
+// A 64-key tile of a [L][D] bf16 matrix is 4*D such chunks, i.e. 4*D/64 spans
+// of 1 KB; chunk i of the tile is LDS byte 16*i = plane i/256, row (i%256)/4,
+// physical slot i%4, holding logical slot (i%4) ^ plane_swz(row).
 //
 // The copy is issued with inline assembly on purpose: the compiler cannot
 // tell that an in-flight copy into one buffer does not alias the operand
@@ -102,28 +91,20 @@ __device__ __forceinline__ uint32_t dma_src_offset(int i, int key_row_limit) {
 // before the first LDS read that follows it, serialising the pipeline.  The
 // kernel orders the buffers itself: s_waitcnt vmcnt(0) and a barrier end
 // every iteration, before any copied tile is read or a buffer is refilled.
-__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
+__device__ __forceinline__ void lds_dma16(const char* sbase, uint32_t voff, uint32_t lds_addr) {
   asm volatile(
-      "s_mov_b32 m0, %1\n\t"
+      "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
+      "global_load_lds_dwordx4 %0, %1"
       :
-      : "v"(gptr), "s"(lds_addr)
+      : "v"(voff), "s"(sbase), "s"(lds_addr)
       : "memory", "m0");
 }
 
-template <int D, int NW>
-__device__ __forceinline__ void dma_tile(const char* tile_src, const uint32_t* src_off,
-                                         uint16_t* lds, int wave_u) {
-  constexpr int SPANS = kTile * D * 2 / 1024;
-  const uint32_t lds_base = (uint32_t)(size_t)(lds_void_t*)lds;  // LDS byte address
-#pragma unroll
-  for (int i = 0; i < SPANS / NW; ++i) {
-    const int span = wave_u + NW * i;
-    lds_dma16(tile_src + src_off[i],
-              __builtin_amdgcn_readfirstlane(lds_base + span * 1024));
-  }
-}
+template <bool B>
+struct CopyFlag {
+  static constexpr bool value = B;
+};
 
 __device__ __forceinline__ void wait_dma() {
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
@@ -216,11 +197,18 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                       : u32x4{0u, 0u, 0u, 0u};
   }
 
-  // Per-lane DMA source offsets of a full tile (rows past L are clamped in
-  // the tail tile only).
-  uint32_t src_full[NI];
+  // DMA instruction i of wave w fills span w + NW*i of a tile: its lanes
+  // cover key row 16*(span%4) + lane/4 of plane span/4, and lane l's source is
+  // the logical 16-byte slot that the swizzle stores at physical slot l%4.
+  int dma_row[NI];
+  uint32_t dma_col[NI];
 #pragma unroll
-  for (int i = 0; i < NI; ++i) src_full[i] = dma_src_offset<D>((wave_u + NW * i) * 64 + lane, 63);
+  for (int i = 0; i < NI; ++i) {
+    const int span = wave_u + NW * i;
+    dma_row[i] = 16 * (span & 3) + (lane >> 2);
+    dma_col[i] = static_cast<uint32_t>((span >> 2) * 64 +
+                                       16 * ((lane & 3) ^ plane_swz(dma_row[i])));
+  }
 
   // Lane-constant LDS byte offsets of the operand reads.
   //  K (A operand of S^T = K Q^T): row 32*st + n, slot 2*(kc&1) + g of plane kc/2.
@@ -241,21 +229,32 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   auto tile_key0 = [&](int t) {
     return __builtin_amdgcn_readfirstlane(static_cast<int>(tiles[t]) * kTile);
   };
-  auto issue = [&](const char* src, int t, uint16_t* lds) {
+  // Source offsets of tile t's copy; rows past L (tail tile only) repeat
+  // row L-1, whose values the -inf mask discards.
+  auto prep = [&](const char* src, int t, uint32_t* off) {
     const int key0 = tile_key0(t);
-    const char* base = src + static_cast<size_t>(key0) * D * 2;
-    if (key0 + kTile <= L) {
-      dma_tile<D, NW>(base, src_full, lds, wave_u);
-    } else {
-      uint32_t src_tail[NI];
+    const int limit = min(kTile - 1, L - 1 - key0);
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
-        src_tail[i] = dma_src_offset<D>((wave_u + NW * i) * 64 + lane, L - 1 - key0);
-      dma_tile<D, NW>(base, src_tail, lds, wave_u);
-    }
+    for (int i = 0; i < NI; ++i)
+      off[i] = static_cast<uint32_t>(min(dma_row[i], limit) * (D * 2)) + dma_col[i];
+    return src + static_cast<size_t>(key0) * D * 2;
+  };
+  auto dma = [&](const char* base, const uint32_t* off, uint16_t* lds, int i) {
+    const uint32_t lds_base = (uint32_t)(size_t)(lds_void_t*)lds;  // LDS byte address
+    lds_dma16(base, off[i], __builtin_amdgcn_readfirstlane(lds_base + (wave_u + NW * i) * 1024));
+  };
+  auto issue = [&](const char* src, int t, uint16_t* lds) {
+    uint32_t off[NI];
+    const char* base = prep(src, t, off);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) dma(base, off, lds, i);
   };
   // S^T of one tile: rows 0..31 in s0, 32..63 in s1.
-  auto qk = [&](const uint16_t* Kt, f32x16& s0, f32x16& s1) {
+  // The NI copy instructions of the next K tile are spread over the k-steps
+  // (one every NW/2 steps) so that no wave stalls on a full memory queue in
+  // front of its matrix instructions.
+  auto qk = [&](auto with_copy, const uint16_t* Kt, f32x16& s0, f32x16& s1,
+                const char* dbase, const uint32_t* doff, uint16_t* dlds) {
     const char* Kb = reinterpret_cast<const char*>(Kt);
     s0 = zero16();
     s1 = zero16();
@@ -266,6 +265,9 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       const u32x4 a1 = *reinterpret_cast<const u32x4*>(Kb + (kc >> 1) * 4096 + 2048 + off);
       s0 = mfma32x32x16(a0, qf[kc], s0);
       s1 = mfma32x32x16(a1, qf[kc], s1);
+      if constexpr (decltype(with_copy)::value) {
+        if (kc % (KC / NI) == KC / NI - 1) dma(dbase, doff, dlds, kc / (KC / NI));
+      }
     }
   };
   // Keys past L get -inf, then the lane-local row max.
@@ -305,12 +307,16 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   wait_dma();
   __syncthreads();
   if (T > 0) {
-    qk(Ks[0], sc0, sc1);
+    qk(CopyFlag<false>{}, Ks[0], sc0, sc1, nullptr, nullptr, nullptr);
     mx_cur = mask_and_max(sc0, sc1, tile_key0(0));
   }
   for (int t = 0; t < T; ++t) {
-    if (t + 2 < T) issue(kh, t + 2, Ks[t & 1]);
-    if (t + 1 < T) issue(vh, t + 1, Vs[(t + 1) & 1]);
+    // Copies of K(t+2) and V(t+1); past the end of the list the last tile is
+    // copied again into the free buffer, which keeps the loop free of
+    // branches around the copies.
+    uint32_t koff[NI], voff[NI];
+    const char* kbase = prep(kh, min(t + 2, T - 1), koff);
+    const char* vbase = prep(vh, min(t + 1, T - 1), voff);
     const float mx = max_halves(mx_cur) * c;
     if (__any(mx > m + kRescaleSlack)) {
       const float m_new = fmaxf(m, mx);
@@ -325,7 +331,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     // S(t+1) on the matrix cores (computed on stale data in the last
     // iteration and discarded) while the VALUs form P(t).
     f32x16 sn0, sn1;
-    qk(Ks[(t + 1) & 1], sn0, sn1);
+    qk(CopyFlag<true>{}, Ks[(t + 1) & 1], sn0, sn1, kbase, koff, Ks[t & 1]);
     uint32_t pb0[8], pb1[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -358,6 +364,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
             (lds_s16x4_t*)(base + v_off1 / 2)));
         const u32x4 a = {lo.x, lo.y, hi.x, hi.y};
         acc[dt] = mfma32x32x16(a, b, acc[dt]);
+        const int j = mm * DT + dt;
+        if (j % NW == NW - 1) dma(vbase, voff, Vs[(t + 1) & 1], j / NW);
       }
     }
     if (t + 1 < T) mx_cur = mask_and_max(sn0, sn1, tile_key0(t + 1));
