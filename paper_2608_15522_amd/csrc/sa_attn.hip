@@ -101,6 +101,21 @@ __device__ __forceinline__ void lds_dma16(const char* sbase, uint32_t voff, uint
       : "memory", "m0");
 }
 
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSgValu = 0x002, kSgMfma = 0x008, kSgDsRead = 0x100;
+#ifndef SA_SCHED_GROUPS
+#define SA_SCHED_GROUPS 0
+#endif
+#ifndef SA_SG_QK
+#define SA_SG_QK 6
+#endif
+#ifndef SA_SG_PV
+#define SA_SG_PV 2
+#endif
+constexpr bool kSchedGroups = SA_SCHED_GROUPS != 0;
+constexpr int kSgValuQK = SA_SG_QK;  // VALU instructions after each QK^T MFMA
+constexpr int kSgValuPV = SA_SG_PV;  // VALU instructions after each PV MFMA
+
 template <bool B>
 struct CopyFlag {
   static constexpr bool value = B;
@@ -140,7 +155,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][TILE_ELEMS];
   __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][TILE_ELEMS];
   __shared__ uint16_t tiles[kMaxBlocks * TPB];  // valid tiles, as key0 / 64
-  __shared__ int ntiles_sh;
+  __shared__ int ntiles_sh, nfull_sh;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -168,21 +183,32 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 
   // Compact the list into 64-key tiles (wave 0): entries outside [0, n_b)
   // are dropped, and so is the second half of a last block of <= 64 keys.
+  // Full tiles keep the list order; the tile that reaches past L (at most
+  // one per list entry of block n_b-1) is placed after all of them, so that
+  // only the last iterations mask keys.
   if (tid < 64) {
-    int base = 0;
+    int nfull = 0, npart = 0;
     const uint64_t below = (1ull << lane) - 1ull;
     for (int i0 = 0; i0 < cnt; i0 += 64) {
       const int i = i0 + lane;
       const int kb = i < cnt ? idx[i] : -1;
       const bool v0 = kb >= 0 && kb < n_b;
       const bool v1 = TPB == 2 && v0 && kb * BLOCK + kTile < L;
-      const uint64_t b0 = __ballot(v0), b1 = __ballot(v1);
-      const int pos = base + __popcll(b0 & below) + __popcll(b1 & below);
-      if (v0) tiles[pos] = static_cast<uint16_t>(kb * TPB);
-      if (v1) tiles[pos + 1] = static_cast<uint16_t>(kb * TPB + 1);
-      base += __popcll(b0) + __popcll(b1);
+      const bool f0 = v0 && kb * BLOCK + kTile <= L;
+      const bool f1 = v1 && kb * BLOCK + 2 * kTile <= L;  // implies f0
+      const uint64_t b0 = __ballot(f0), b1 = __ballot(f1);
+      const int pos = nfull + __popcll(b0 & below) + __popcll(b1 & below);
+      if (f0) tiles[pos] = static_cast<uint16_t>(kb * TPB);
+      if (f1) tiles[pos + 1] = static_cast<uint16_t>(kb * TPB + 1);
+      nfull += __popcll(b0) + __popcll(b1);
+      npart += __popcll(__ballot(v0 && !f0)) + __popcll(__ballot(v1 && !f1));
     }
-    if (lane == 0) ntiles_sh = base;
+    for (int j = lane; j < npart; j += 64)
+      tiles[nfull + j] = static_cast<uint16_t>((L - 1) / kTile);
+    if (lane == 0) {
+      ntiles_sh = nfull + npart;
+      nfull_sh = nfull;
+    }
   }
 
   const uint16_t* qh = q + static_cast<size_t>(pair) * L * D;
@@ -226,6 +252,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 
   __syncthreads();  // the tile list is visible
   const int T = ntiles_sh;
+  const int T_full = nfull_sh;
   auto tile_key0 = [&](int t) {
     return __builtin_amdgcn_readfirstlane(static_cast<int>(tiles[t]) * kTile);
   };
@@ -270,15 +297,10 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       }
     }
   };
-  // Keys past L get -inf, then the lane-local row max.
-  auto mask_and_max = [&](f32x16& s0, f32x16& s1, int key0) {
-    if (key0 + kTile > L) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        if (key0 + crow(i, g) >= L) s0[i] = -INFINITY;
-        if (key0 + 32 + crow(i, g) >= L) s1[i] = -INFINITY;
-      }
-    }
+  // Lane-local row max over the 64 keys of a tile.  Rows past L were copied
+  // from row L-1 of the same tile, so they repeat a valid logit and leave
+  // the max unchanged; their probabilities are zeroed when P is formed.
+  auto tile_max = [&](const f32x16& s0, const f32x16& s1) {
     float mx = s0[0];
 #pragma unroll
     for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
@@ -297,7 +319,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 
   // Pipeline: K runs one tile ahead of V.  On entry to iteration t, K(t+1)
   // and V(t) are in LDS and S(t) is in registers.
-  f32x16 sc0 = zero16(), sc1 = zero16();
+  f32x16 sc0 = zero16(), sc1 = zero16(), sn_0, sn_1;
   float mx_cur = -INFINITY;
   if (T > 0) {
     issue(kh, 0, Ks[0]);
@@ -308,12 +330,15 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   __syncthreads();
   if (T > 0) {
     qk(CopyFlag<false>{}, Ks[0], sc0, sc1, nullptr, nullptr, nullptr);
-    mx_cur = mask_and_max(sc0, sc1, tile_key0(0));
+    mx_cur = tile_max(sc0, sc1);
   }
-  for (int t = 0; t < T; ++t) {
-    // Copies of K(t+2) and V(t+1); past the end of the list the last tile is
-    // copied again into the free buffer, which keeps the loop free of
-    // branches around the copies.
+  __syncthreads();  // every wave has read K(0) before iteration 0 refills its buffer
+  // One iteration: the copies of K(t+2) and V(t+1) run under S(t+1) = QK^T
+  // on the matrix cores, P(t) on the VALUs, and PV(t).  Past the end of the
+  // list the last tile is copied again into the free buffer, which keeps the
+  // iteration free of branches around the copies.  `tail` marks iterations
+  // whose tile t reaches past L: only they zero P for rows past L.
+  auto iteration = [&](int t, auto tail) {
     uint32_t koff[NI], voff[NI];
     const char* kbase = prep(kh, min(t + 2, T - 1), koff);
     const char* vbase = prep(vh, min(t + 1, T - 1), voff);
@@ -333,12 +358,26 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     f32x16 sn0, sn1;
     qk(CopyFlag<true>{}, Ks[(t + 1) & 1], sn0, sn1, kbase, koff, Ks[t & 1]);
     uint32_t pb0[8], pb1[8];
+    if constexpr (decltype(tail)::value) {
+      const int kv = L - tile_key0(t);  // valid rows of this tile
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      pb0[i] = pack_bf16x2(fast_exp2(fmaf(sc0[2 * i], c, -m)),
-                           fast_exp2(fmaf(sc0[2 * i + 1], c, -m)));
-      pb1[i] = pack_bf16x2(fast_exp2(fmaf(sc1[2 * i], c, -m)),
-                           fast_exp2(fmaf(sc1[2 * i + 1], c, -m)));
+      for (int i = 0; i < 8; ++i) {
+        const float p0 = crow(2 * i, g) < kv ? fast_exp2(fmaf(sc0[2 * i], c, -m)) : 0.f;
+        const float p1 = crow(2 * i + 1, g) < kv ? fast_exp2(fmaf(sc0[2 * i + 1], c, -m)) : 0.f;
+        const float p2 = 32 + crow(2 * i, g) < kv ? fast_exp2(fmaf(sc1[2 * i], c, -m)) : 0.f;
+        const float p3 =
+            32 + crow(2 * i + 1, g) < kv ? fast_exp2(fmaf(sc1[2 * i + 1], c, -m)) : 0.f;
+        pb0[i] = pack_bf16x2(p0, p1);
+        pb1[i] = pack_bf16x2(p2, p3);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        pb0[i] = pack_bf16x2(fast_exp2(fmaf(sc0[2 * i], c, -m)),
+                             fast_exp2(fmaf(sc0[2 * i + 1], c, -m)));
+        pb1[i] = pack_bf16x2(fast_exp2(fmaf(sc1[2 * i], c, -m)),
+                             fast_exp2(fmaf(sc1[2 * i + 1], c, -m)));
+      }
     }
     // row sum of the bf16 probabilities that the PV product uses
 #pragma unroll
@@ -368,12 +407,161 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
         if (j % NW == NW - 1) dma(vbase, voff, Vs[(t + 1) & 1], j / NW);
       }
     }
-    if (t + 1 < T) mx_cur = mask_and_max(sn0, sn1, tile_key0(t + 1));
+    // max of S(t+1); in the last iteration it is not used
+    mx_cur = tile_max(sn0, sn1);
     sc0 = sn0;
     sc1 = sn1;
+    // Issue order: the QK^T MFMAs of S(t+1), each followed by a share of the
+    // VALU work that forms P(t), then the PV MFMAs, each preceded by its two
+    // transposing reads and followed by a share of the max of S(t+1).
+    if constexpr (kSchedGroups) {
+      __builtin_amdgcn_sched_group_barrier(kSgDsRead, 4, 0);
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgValu, kSgValuQK, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgValu, kSgValuQK, 0);
+        if (kc + 2 < KC) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < 4 * DT; ++j) {
+        __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgValu, kSgValuPV, 0);
+      }
+    }
     wait_dma();
     __syncthreads();
+  };
+  // Steady-state iteration for t + 2 < T_full (tiles t, t+1 and t+2 hold 64
+  // keys each).  The issue order is fixed by scheduling barriers so that
+  // every MFMA is followed by a share of the VALU work: in the QK^T phase
+  // (S(t+1) into n0/n1) one bf16 pair of P(t) per MFMA; in the PV phase the
+  // row sums of P(t), then the row max of S(t+1).  Operand reads run two
+  // MFMAs ahead, and the NI copies of each matrix are spread over its phase.
+  uint32_t dma_full[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) dma_full[i] = static_cast<uint32_t>(dma_row[i] * (D * 2)) + dma_col[i];
+  auto main_iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
+    const char* kbase = kh + static_cast<size_t>(tile_key0(t + 2)) * D * 2;
+    const char* vbase = vh + static_cast<size_t>(tile_key0(t + 1)) * D * 2;
+    const float mx = max_halves(mx_cur) * c;
+    if (__any(mx > m + kRescaleSlack)) {
+      const float m_new = fmaxf(m, mx);
+      const float alpha = fast_exp2(m - m_new);
+      m = m_new;
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
+    }
+    const char* Kb = reinterpret_cast<const char*>(Ks[(t + 1) & 1]);
+    const lds_u16_t* Vb = (const lds_u16_t*)Vs[t & 1];
+    uint16_t* kdst = Ks[t & 1];
+    uint16_t* vdst = Vs[(t + 1) & 1];
+    auto kread = [&](int kc, u32x4* dst) {
+      const int off = (kc & 1) ? k_off1 : k_off0;
+      dst[0] = *reinterpret_cast<const u32x4*>(Kb + (kc >> 1) * 4096 + off);
+      dst[1] = *reinterpret_cast<const u32x4*>(Kb + (kc >> 1) * 4096 + 2048 + off);
+    };
+    auto vread = [&](int j, u32x4& dst) {
+      const lds_u16_t* base = Vb + ((j % DT) * 4096 + (j / DT) * 1024) / 2;
+      const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4_t*)(base + v_off0 / 2)));
+      const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s16x4_t*)(base + v_off1 / 2)));
+      dst = u32x4{lo.x, lo.y, hi.x, hi.y};
+    };
+    // ---- QK^T phase: S(t+1) on the matrix cores, P(t) on the VALUs
+    constexpr int NA = 2 * KC;          // MFMAs
+    constexpr int PPA = 16 / NA;        // bf16 pairs of P per MFMA
+    u32x4 ka[3][2];
+    uint32_t pb[16];
+    kread(0, ka[0]);
+    kread(1, ka[1]);
+    n0 = zero16();
+    n1 = zero16();
+#pragma unroll
+    for (int st = 0; st < NA; ++st) {
+      const int kc = st >> 1;
+      if ((st & 1) == 0 && kc + 2 < KC) kread(kc + 2, ka[(kc + 2) % 3]);
+      if (st & 1)
+        n1 = mfma32x32x16(ka[kc % 3][1], qf[kc], n1);
+      else
+        n0 = mfma32x32x16(ka[kc % 3][0], qf[kc], n0);
+#pragma unroll
+      for (int u = 0; u < PPA; ++u) {
+        const int pk = st * PPA + u;  // 0..7 from c0, 8..15 from c1
+        const f32x16& src = pk < 8 ? c0 : c1;
+        const int e = 2 * (pk & 7);
+        pb[pk] = pack_bf16x2(fast_exp2(fmaf(src[e], c, -m)), fast_exp2(fmaf(src[e + 1], c, -m)));
+      }
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        if (i * NA / NI == st) {
+          const uint32_t la = (uint32_t)(size_t)(lds_void_t*)kdst;
+          lds_dma16(kbase, dma_full[i],
+                    __builtin_amdgcn_readfirstlane(la + (wave_u + NW * i) * 1024));
+        }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- PV phase: O^T += V(t)^T P(t)^T; row sums of P(t), row max of S(t+1)
+    constexpr int NB = 4 * DT;          // MFMAs
+    constexpr int VB = 32 / NB;         // VALU ops per MFMA
+    u32x4 va[3];
+    vread(0, va[0]);
+    vread(1, va[1]);
+    float mxn = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      if (j + 2 < NB) vread(j + 2, va[(j + 2) % 3]);
+      const int mm = j / DT, dt = j % DT;
+      const int h = (mm & 1) * 4 + (mm < 2 ? 0 : 8);
+      const u32x4 b = {pb[h], pb[h + 1], pb[h + 2], pb[h + 3]};
+      acc[dt] = mfma32x32x16(va[j % 3], b, acc[dt]);
+#pragma unroll
+      for (int u = 0; u < VB; ++u) {
+        const int w = j * VB + u;  // 0..15: row sums, 16..31: max pairs
+        if (w < 16) {
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb[w]), ones,
+                                                 lsum, false);
+        } else {
+          const int e = w - 16;  // pair e: elements 2e, 2e+1 of n0 (e < 8) or n1
+          const f32x16& src = e < 8 ? n0 : n1;
+          mxn = fmaxf(mxn, src[2 * (e & 7)]);
+          mxn = fmaxf(mxn, src[2 * (e & 7) + 1]);
+          asm volatile("" : "+v"(mxn));  // keeps this share of the max in its slot
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        if (i * NB / NI == j) {
+          const uint32_t la = (uint32_t)(size_t)(lds_void_t*)vdst;
+          lds_dma16(vbase, dma_full[i],
+                    __builtin_amdgcn_readfirstlane(la + (wave_u + NW * i) * 1024));
+        }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    mx_cur = mxn;
+    wait_dma();
+    __syncthreads();
+  };
+
+  const int T_main = T_full > 2 ? T_full - 2 : 0;
+  int t = 0;
+  for (; t + 1 < T_main; t += 2) {
+    main_iter(t, sc0, sc1, sn_0, sn_1);
+    main_iter(t + 1, sn_0, sn_1, sc0, sc1);
   }
+  if (t < T_main) {
+    main_iter(t, sc0, sc1, sn_0, sn_1);
+    sc0 = sn_0;
+    sc1 = sn_1;
+    ++t;
+  }
+  for (; t < T; ++t) iteration(t, CopyFlag<true>{});
 
   const float ltot = lsum + swap_halves(lsum);
   const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
