@@ -474,7 +474,10 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
           (lds_s16x4_t*)(base + v_off1 / 2)));
       dst = u32x4{lo.x, lo.y, hi.x, hi.y};
     };
-    // ---- QK^T phase: S(t+1) on the matrix cores, P(t) on the VALUs
+    // ---- QK^T phase: S(t+1) on the matrix cores, P(t) on the VALUs.  The
+    // wave issues at raised priority here, where most of its VALU work lies,
+    // and at normal priority in the PV phase.
+    __builtin_amdgcn_s_setprio(1);
     constexpr int NA = 2 * KC;          // MFMAs
     constexpr int PPA = 16 / NA;        // bf16 pairs of P per MFMA
     u32x4 ka[3][2];
@@ -508,6 +511,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       __builtin_amdgcn_sched_barrier(0);
     }
     // ---- PV phase: O^T += V(t)^T P(t)^T; row sums of P(t), row max of S(t+1)
+    __builtin_amdgcn_s_setprio(0);
     constexpr int NB = 4 * DT;          // MFMAs
     constexpr int VB = 32 / NB;         // VALU ops per MFMA
     u32x4 va[3];
@@ -545,6 +549,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       __builtin_amdgcn_sched_barrier(0);
     }
     mx_cur = mxn;
+    __builtin_amdgcn_s_setprio(0);
     wait_dma();
     __syncthreads();
   };

@@ -170,98 +170,89 @@ __global__ void lse_combine_kernel(const float2* __restrict__ part,
 }
 
 // ---- K2 ---------------------------------------------------------------------
-constexpr int kColKeys = 128;  // video keys per K2 workgroup
+// Column mass of one (batch, head) pair over a chunk of kColChunk video keys.
+// 8 waves; wave w owns audio queries 64*w .. 64*w+63 of the current 512-query
+// slab (two 32-row MFMA blocks), so every K operand read from LDS feeds two
+// MFMAs.  S = Q^a K^v^T puts one video key per lane column: the lane sums
+// exp2(S*c - lse) over its query rows and adds the result to its own slot of
+// an LDS partial array (one writer per slot, so the order is fixed); the 16
+// partials of a key (2 lane halves x 8 waves) are added in order at the end.
+// Query rows past L_a carry lse = +inf, so their probabilities are exactly 0;
+// keys past L_v only reach their own columns, which are not written.
+constexpr int kColChunk = 512;   // video keys per K2 workgroup
+constexpr int kColWaves = 8;     // 64 audio queries per wave
 
 template <int D>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(kColWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
                    const uint16_t* __restrict__ k_v,
                    const float* __restrict__ lse2, float* __restrict__ colmass,
                    int H, int L_v, int L_a, float c) {
-  constexpr int NT = 1024, KC = D / 16, CPR = D / 8;
-  constexpr int CH = (kColKeys * CPR + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kColKeys * D];
-  __shared__ float red[16][2][kColKeys];
-  const int kblk = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
-  const int ngroup = gridDim.y;
+  constexpr int NT = kColWaves * 64, KC = D / 16, CPR = D / 8;
+  constexpr int CH = (kCT * CPR + NT - 1) / NT;   // 16-byte chunks per thread per tile
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kCT * D];
+  __shared__ float red[kColWaves * 2][kColChunk];
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 5, n = lane & 31;
-  const int key0 = kblk * kColKeys;
-  const int h0 = hg * kHeadGroup;
-  const int h1 = min(h0 + kHeadGroup, H);
+  const int key0 = chunk * kColChunk;
+  const int key_end = min(key0 + kColChunk, L_v);
+  const size_t pair = static_cast<size_t>(b) * H + h;
+  const uint16_t* kh = k_v + pair * L_v * D;
+  const uint16_t* qh = q_a + pair * L_a * D;
+  const float* lh = lse2 + pair * L_a;
   const int nslab = ceil_div(L_a, kQSlab);
-  const int nsteps = (h1 - h0) * nslab;
+  const int ntiles = ceil_div(key_end - key0, kCT);
+  float* myred = red[2 * wave + g];
+  for (int i = n; i < kColChunk; i += 32) myred[i] = 0.f;
 
-  auto load_k = [&](int step, u32x4* reg) {
-    const int h = h0 + step / nslab;
-    const uint16_t* kh = k_v + (static_cast<size_t>(b) * H + h) * L_v * D;
+  for (int slab = 0; slab < nslab; ++slab) {
+    const int jb = slab * kQSlab + wave * 64;   // first query row of this wave
+    u32x4 qf[2][KC];
+    load_qfrag<D>(qh, jb + n, L_a, g, qf[0]);
+    load_qfrag<D>(qh, jb + 32 + n, L_a, g, qf[1]);
+    float lr[2][16];
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int qq = threadIdx.x + NT * i;
-      const int row = qq / CPR, cc = qq % CPR;
-      reg[i] = (qq < kColKeys * CPR && key0 + row < L_v)
-                   ? ldg16(kh + static_cast<size_t>(key0 + row) * D + cc * 8)
-                   : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-  auto store_k = [&](uint16_t* lds, const u32x4* reg) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int qq = threadIdx.x + NT * i;
-      if (qq < kColKeys * CPR) {
-        const int row = qq / CPR, cc = qq % CPR;
-        stg16(lds + row * D + ((cc ^ (row & (CPR - 1))) * 8), reg[i]);
-      }
-    }
-  };
-
-  float colacc[4] = {0.f, 0.f, 0.f, 0.f};
-  u32x4 reg[CH];
-  load_k(0, reg);
-  store_k(Ks[0], reg);
-  __syncthreads();
-  for (int step = 0; step < nsteps; ++step) {
-    const int buf = step & 1;
-    const int h = h0 + step / nslab;
-    const int slab = step % nslab;
-    if (step + 1 < nsteps) load_k(step + 1, reg);
-    const int jbase = slab * kQSlab + wave * 32;
-    if (jbase < L_a) {
-      const size_t pair = static_cast<size_t>(b) * H + h;
-      u32x4 qf[KC];
-      load_qfrag<D>(q_a + pair * L_a * D, jbase + n, L_a, g, qf);
-      // log-sum-exp of the 16 audio-query rows this lane holds; rows past
-      // L_a get +inf so that their probabilities are exactly 0
-      float lr[16];
+    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int jj = jbase + crow(i, g);
-        lr[i] = jj < L_a ? lse2[pair * L_a + jj] : INFINITY;
+        const int jj = jb + 32 * qb + crow(i, g);
+        lr[qb][i] = jj < L_a ? lh[jj] : INFINITY;
       }
+    u32x4 reg[CH];
+    load_rows_to_regs<D, NT>(kh, key0, key_end, reg);
+    __syncthreads();  // the previous slab is done with both buffers
+    store_rows_to_lds<D, NT>(Ks[0], reg);
+    __syncthreads();
+#pragma unroll 1
+    for (int t = 0; t < ntiles; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < ntiles) load_rows_to_regs<D, NT>(kh, key0 + (t + 1) * kCT, key_end, reg);
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        f32x16 s = zero16();
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16 s0 = zero16(), s1 = zero16();
 #pragma unroll
-        for (int kc = 0; kc < KC; ++kc)
-          s = mfma32x32x16(qf[kc], lds_frag<D>(Ks[buf], 32 * st + n, kc, g), s);
+        for (int kc = 0; kc < KC; ++kc) {
+          const u32x4 kf = lds_frag<D>(Ks[buf], 32 * kb + n, kc, g);
+          s0 = mfma32x32x16(qf[0][kc], kf, s0);
+          s1 = mfma32x32x16(qf[1][kc], kf, s1);
+        }
         float cs = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) cs += fast_exp2(fmaf(s[i], c, -lr[i]));
-        colacc[st] += cs;
+        for (int i = 0; i < 16; ++i)
+          cs += fast_exp2(fmaf(s0[i], c, -lr[0][i])) + fast_exp2(fmaf(s1[i], c, -lr[1][i]));
+        myred[t * kCT + 32 * kb + n] += cs;
       }
+      if (t + 1 < ntiles) store_rows_to_lds<D, NT>(Ks[buf ^ 1], reg);
+      __syncthreads();
     }
-    if (step + 1 < nsteps) store_k(Ks[buf ^ 1], reg);
-    __syncthreads();
   }
-#pragma unroll
-  for (int st = 0; st < 4; ++st) red[wave][g][32 * st + n] = colacc[st];
   __syncthreads();
-  if (threadIdx.x < kColKeys) {
-    const int kk = threadIdx.x;
+  for (int kk = threadIdx.x; kk < kColChunk; kk += NT) {
     float sum = 0.f;
-    for (int w = 0; w < 16; ++w) sum += red[w][0][kk] + red[w][1][kk];
-    if (key0 + kk < L_v)
-      colmass[(static_cast<size_t>(b) * ngroup + hg) * L_v + key0 + kk] = sum;
+#pragma unroll
+    for (int w = 0; w < kColWaves * 2; ++w) sum += red[w][kk];
+    if (key0 + kk < L_v) colmass[pair * L_v + key0 + kk] = sum;
   }
 }
 
@@ -379,19 +370,20 @@ v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
 }
 
 // ---- finalize ---------------------------------------------------------------
-// sal_v_tok / sal_v_blk from per-group column mass: grid (n_b, B), block
+// sal_v_tok / sal_v_blk from column-mass partials [B][nsum][L_v] (per head,
+// or one partial holding every head), summed in order: grid (n_b, B), block
 // threads = `block` (one per token of the video block).
 __global__ void __launch_bounds__(128)
 a2v_finalize_kernel(const float* __restrict__ colmass, float* __restrict__ sal_v_tok,
-                    float* __restrict__ sal_v_blk, int L_v, int ngroup,
+                    float* __restrict__ sal_v_blk, int L_v, int nsum,
                     float inv_norm, int accumulate) {
   __shared__ float red[128];
   const int c = blockIdx.x, b = blockIdx.y, n_b = gridDim.x;
   const int i = c * blockDim.x + threadIdx.x;
   float v = 0.f;
   if (i < L_v) {
-    for (int gi = 0; gi < ngroup; ++gi)
-      v += colmass[(static_cast<size_t>(b) * ngroup + gi) * L_v + i];
+    for (int gi = 0; gi < nsum; ++gi)
+      v += colmass[(static_cast<size_t>(b) * nsum + gi) * L_v + i];
     v *= inv_norm;
     if (sal_v_tok != nullptr) {
       float* dst = sal_v_tok + static_cast<size_t>(b) * L_v + i;
@@ -510,7 +502,6 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
   const int P = B * H;
   const int nchunk = ceil_div(L_v, kLseChunk);
   const int nslab = ceil_div(L_a, kQSlab);
-  const int ngroup = ceil_div(H, kHeadGroup);
   float2* lse_part = reinterpret_cast<float2*>(ws + lay.lse_part);
   float* lse_a = reinterpret_cast<float*>(ws + lay.lse_a);
   float* colmass = reinterpret_cast<float*>(ws + lay.colmass);
@@ -519,11 +510,11 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
   const size_t nlse = static_cast<size_t>(P) * L_a;
   hipLaunchKernelGGL(lse_combine_kernel, dim3((nlse + 255) / 256), dim3(256), 0, s,
                      lse_part, lse_a, P, L_a, nchunk);
-  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColKeys), ngroup, B),
-                     dim3(1024), 0, s, q_a, k_v, lse_a, colmass, H, L_v, L_a, c);
+  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColChunk), H, B),
+                     dim3(kColWaves * 64), 0, s, q_a, k_v, lse_a, colmass, H, L_v, L_a, c);
   const int n_b = ceil_div(L_v, block);
   hipLaunchKernelGGL(a2v_finalize_kernel, dim3(n_b, B), dim3(block), 0, s, colmass,
-                     sal_v_tok, sal_v_blk, L_v, ngroup,
+                     sal_v_tok, sal_v_blk, L_v, H,
                      1.0f / (static_cast<float>(H) * static_cast<float>(L_a)), accumulate);
   if (q_v != nullptr) {
     float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);

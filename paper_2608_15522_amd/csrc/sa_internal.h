@@ -12,7 +12,6 @@ namespace sa {
 // Tunables fixed at build time.
 constexpr int kLseChunk = 1024;   // video keys per a->v log-sum-exp partial
 constexpr int kQSlab = 512;       // queries per 16-wave workgroup slab
-constexpr int kHeadGroup = 4;     // heads per a->v column-mass partial
 constexpr int kV2aChunk = 512;    // video queries per v->a workgroup
 constexpr int kMaxBlocks = 2048;  // largest supported n_b
 
@@ -22,7 +21,7 @@ inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 struct CrossWs {
   size_t lse_part;   // float2 [B,H,nchunk,L_a]  (m, l) partials, bf16 path
   size_t lse_a;      // float  [B,H,L_a]         a->v log2-sum-exp
-  size_t colmass;    // float  [B,ngroup,L_v]    per head-group column mass
+  size_t colmass;    // float  [B,H,L_v]         per-head a->v column mass
   size_t lse_v;      // float  [B,H,L_v]         v->a log2-sum-exp, f32 path
   size_t v2a_part;   // float  [B,H,nchunk3,L_a] v->a column-mass partials
   size_t v2a_head;   // float  [B,H,L_a]         the same summed over chunks
@@ -32,12 +31,11 @@ struct CrossWs {
 inline CrossWs cross_ws_layout(int B, int H, int L_v, int L_a) {
   CrossWs w{};
   const size_t nchunk = (L_v + kLseChunk - 1) / kLseChunk;
-  const size_t ngroup = (H + kHeadGroup - 1) / kHeadGroup;
   const size_t nchunk3 = (L_v + kV2aChunk - 1) / kV2aChunk;
   size_t off = 0;
   w.lse_part = off; off += align_up(sizeof(float) * 2 * B * H * nchunk * L_a);
   w.lse_a = off;    off += align_up(sizeof(float) * B * H * L_a);
-  w.colmass = off;  off += align_up(sizeof(float) * B * ngroup * L_v);
+  w.colmass = off;  off += align_up(sizeof(float) * B * H * L_v);
   w.lse_v = off;    off += align_up(sizeof(float) * B * H * L_v);
   w.v2a_part = off; off += align_up(sizeof(float) * B * H * nchunk3 * L_a);
   w.v2a_head = off; off += align_up(sizeof(float) * B * H * L_a);
