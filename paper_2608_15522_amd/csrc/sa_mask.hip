@@ -7,12 +7,14 @@
 // K5 block_pool: per (b,h, block) the mean of Q and of K over the valid
 //    tokens of the block, accumulated in fp64 (16-byte loads, fixed-order LDS
 //    reduction); the sums of bf16/fp32 inputs are exact.
-// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and up to 8 query
+// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and a group of query
 //    blocks, the pooled scores G = scale * qbar kbar^T by fp64 FMA (a few
 //    hundred MFLOP per layer; fp32 would misrank scores closer than ~1e-6,
 //    and pooled-score gaps are that small), then per row either the full list
-//    (protected row) or the top-k_keep of an LDS bitonic sort of the row's
-//    keys, compacted into an ascending list with a workgroup prefix sum.
+//    (protected row) or the top-k_keep blocks: one wave finds the k-th
+//    smallest order key (value descending, index ascending) by a bitwise
+//    search with ballots and compacts the blocks at or below it into an
+//    ascending list.
 #include "sa_device.h"
 #include "sa_internal.h"
 
@@ -107,124 +109,158 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
 }
 
 // ---- K6 ---------------------------------------------------------------------
-constexpr int kMaskThreads = 256;
-constexpr int kRowsPerWg = 8;  // upper bound of the rows handled per workgroup
+constexpr int kMaskThreads = 256;  // 4 waves
 
-// Rows per workgroup so that the per-row key arrays take at most 32 KB.
-inline int mask_rows_per_wg(int n_pad) {
-  const int r = 4096 / n_pad;
-  return r < 1 ? 1 : (r > kRowsPerWg ? kRowsPerWg : r);
+// k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 keys held
+// by one wave (E per lane), all distinct: bits are fixed from the top, each
+// step counting the keys that share the fixed prefix and have a 0 next.
+template <int E>
+__device__ __forceinline__ uint64_t wave_kth_smallest(const uint64_t* keys, int k) {
+  uint64_t prefix = 0;
+  int below = 0;
+  for (int bit = 63; bit >= 0; --bit) {
+    const uint64_t hi = ~((2ull << bit) - 1ull);  // bits above `bit`
+    const uint64_t sel = hi | (1ull << bit);
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) cnt += __popcll(__ballot((keys[e] & sel) == prefix));
+    if (below + cnt < k) {
+      below += cnt;
+      prefix |= 1ull << bit;
+    }
+  }
+  return prefix;
 }
 
-// Dynamic LDS: keys[rows][n_pad] u64 | qbar rows [rows][D] f64 |
-// sel[n_pad] u8 | scan[kMaskThreads] i32.
-template <int D>
+// Grid (ceil(n_b / ROWS), P), 256 threads; template E = n_pad / 64 (n_pad the
+// next power of two >= n_b, at least 64).  Column col = 64*e + lane of a row
+// lives in register e of lane `lane`.  Each wave owns RW rows.
+template <int D, int E>
 __global__ void __launch_bounds__(kMaskThreads)
 mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kbar,
-                  const uint8_t* __restrict__ prot_flag, int H, int n_b,
-                  int n_pad, int rows, int k_keep, double scale,
-                  int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt,
+                  const uint8_t* __restrict__ prot_flag, int H, int n_b, int k_keep,
+                  double scale, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt,
                   uint8_t* __restrict__ mask, float* __restrict__ scores) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint64_t* keys_all = reinterpret_cast<uint64_t*>(smem);
-  double* qs = reinterpret_cast<double*>(keys_all + static_cast<size_t>(rows) * n_pad);
-  uint8_t* sel = reinterpret_cast<uint8_t*>(qs + rows * D);
-  int* scan = reinterpret_cast<int*>(sel + ((n_pad + 15) & ~15));
-
-  const int tid = threadIdx.x;
+  constexpr int NPAD = 64 * E;
+  constexpr int RW = E >= 8 ? 1 : 8 / E;          // rows per wave
+  constexpr int ROWS = 4 * RW;                     // rows per workgroup
+  constexpr int DCH = (8192 / NPAD) < D ? (8192 / NPAD) : D;  // d values per 64 KB stage
+  constexpr int KSS = NPAD + 1;                    // padded row: conflict-free stores
+  constexpr int PER = DCH * NPAD / kMaskThreads;   // staged values per thread
+  __shared__ double ks[DCH * KSS];
+  __shared__ double qs[ROWS * D];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t pair = blockIdx.y;
   const int b = static_cast<int>(pair / H);
-  const int r0 = blockIdx.x * rows;
-  const int nr = min(rows, n_b - r0);
+  const int r0 = blockIdx.x * ROWS;
   const double* qb = qbar + pair * n_b * D;
   const double* kb = kbar + pair * n_b * D;
 
-  for (int e = tid; e < nr * D; e += kMaskThreads) qs[e] = qb[static_cast<size_t>(r0) * D + e];
-  __syncthreads();
-  // pooled scores in fp64, one key block per thread, d-sequential FMA; the
-  // sort keys of every row and the optional fp32 copy of G are written here
-  for (int col = tid; col < n_pad; col += kMaskThreads) {
-    if (col >= n_b) {
-      for (int rr = 0; rr < nr; ++rr) keys_all[rr * n_pad + col] = ~0ull;
-      continue;
+  for (int i = tid; i < ROWS * D; i += kMaskThreads) {
+    const int rr = i / D;
+    qs[i] = r0 + rr < n_b ? qb[static_cast<size_t>(r0) * D + i] : 0.0;
+  }
+  double acc[RW][E];
+#pragma unroll
+  for (int rr = 0; rr < RW; ++rr)
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[rr][e] = 0.0;
+  for (int d0 = 0; d0 < D; d0 += DCH) {
+    // kbar[col][d0 .. d0+DCH) -> ks[dd][col]: every load of the stage is
+    // issued before the first store (DCH consecutive threads read one row)
+    double v[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int i = tid + kMaskThreads * j;
+      const int col = i / DCH, dd = i % DCH;
+      v[j] = col < n_b ? kb[static_cast<size_t>(col) * D + d0 + dd] : 0.0;
     }
-    double acc[kRowsPerWg];
+    __syncthreads();  // the previous stage has been consumed
 #pragma unroll
-    for (int rr = 0; rr < kRowsPerWg; ++rr) acc[rr] = 0.0;
-    const double* kr = kb + static_cast<size_t>(col) * D;
-    for (int e = 0; e < D; ++e) {
-      const double kv = kr[e];
-#pragma unroll
-      for (int rr = 0; rr < kRowsPerWg; ++rr)
-        if (rr < nr) acc[rr] = fma(qs[rr * D + e], kv, acc[rr]);
+    for (int j = 0; j < PER; ++j) {
+      const int i = tid + kMaskThreads * j;
+      ks[(i % DCH) * KSS + i / DCH] = v[j];
     }
+    __syncthreads();
+#pragma unroll 4
+    for (int dd = 0; dd < DCH; ++dd) {
+      double kv[E];
 #pragma unroll
-    for (int rr = 0; rr < kRowsPerWg; ++rr) {
-      if (rr < nr) {
-        const double gval = acc[rr] * scale;
-        keys_all[rr * n_pad + col] = desc_double_asc_index_key(gval, static_cast<uint32_t>(col));
-        if (scores != nullptr)
-          scores[(pair * n_b + r0 + rr) * n_b + col] = static_cast<float>(gval);
+      for (int e = 0; e < E; ++e) kv[e] = ks[dd * KSS + 64 * e + lane];
+#pragma unroll
+      for (int rr = 0; rr < RW; ++rr) {
+        const double qv = qs[(wave * RW + rr) * D + d0 + dd];
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[rr][e] = fma(qv, kv[e], acc[rr][e]);
       }
     }
   }
-  __syncthreads();
 
-  const int per = ceil_div(n_b, kMaskThreads);  // entries per thread in the scan
-  for (int rr = 0; rr < nr; ++rr) {
-    const int r = r0 + rr;
+  const uint64_t below_mask = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int rr = 0; rr < RW; ++rr) {
+    const int r = r0 + wave * RW + rr;
+    if (r >= n_b) break;  // uniform across the wave
     const size_t row = pair * n_b + r;
-    const bool prot = prot_flag != nullptr && prot_flag[static_cast<size_t>(b) * n_b + r] != 0;
     int32_t* out_idx = kv_idx + row * n_b;
+    uint64_t keys[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int col = 64 * e + lane;
+      const double gval = acc[rr][e] * scale;
+      keys[e] = col < n_b ? desc_double_asc_index_key(gval, static_cast<uint32_t>(col)) : ~0ull;
+      if (scores != nullptr && col < n_b) scores[row * n_b + col] = static_cast<float>(gval);
+    }
+    const bool prot = prot_flag != nullptr && prot_flag[static_cast<size_t>(b) * n_b + r] != 0;
     if (prot) {
-      for (int col = tid; col < n_b; col += kMaskThreads) {
+      for (int col = lane; col < n_b; col += 64) {
         out_idx[col] = col;
         if (mask != nullptr) mask[row * n_b + col] = 1;
       }
-      if (tid == 0) kv_cnt[row] = n_b;
-      continue;  // uniform across the workgroup
+      if (lane == 0) kv_cnt[row] = n_b;
+      continue;
     }
-    uint64_t* keys = keys_all + static_cast<size_t>(rr) * n_pad;
-    for (int i = tid; i < n_pad; i += kMaskThreads) sel[i] = 0;
-    bitonic_sort_lds(keys, n_pad);
-    for (int i = tid; i < k_keep; i += kMaskThreads)
-      sel[static_cast<uint32_t>(keys[i] & 0xfffu)] = 1;
-    __syncthreads();
-    // exclusive prefix count of sel over ascending column index
-    const int lo = tid * per, hi = min(lo + per, n_b);
-    int local = 0;
-    for (int i = lo; i < hi; ++i) local += sel[i];
-    scan[tid] = local;
-    __syncthreads();
-    for (int off = 1; off < kMaskThreads; off <<= 1) {
-      const int v = tid >= off ? scan[tid - off] : 0;
-      __syncthreads();
-      scan[tid] += v;
-      __syncthreads();
+    const uint64_t kth = wave_kth_smallest<E>(keys, k_keep);
+    int base = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int col = 64 * e + lane;
+      const bool on = keys[e] <= kth;  // padding keys (~0) are never at or below it
+      const uint64_t m = __ballot(on);
+      if (on) out_idx[base + __popcll(m & below_mask)] = col;
+      base += __popcll(m);
+      if (mask != nullptr && col < n_b) mask[row * n_b + col] = on ? 1 : 0;
     }
-    int pos = scan[tid] - local;
-    for (int i = lo; i < hi; ++i) {
-      if (sel[i]) out_idx[pos++] = i;
-    }
-    for (int i = k_keep + tid; i < n_b; i += kMaskThreads) out_idx[i] = -1;
-    if (mask != nullptr)
-      for (int col = tid; col < n_b; col += kMaskThreads) mask[row * n_b + col] = sel[col];
-    if (tid == 0) kv_cnt[row] = k_keep;
-    __syncthreads();
+    for (int i = k_keep + lane; i < n_b; i += 64) out_idx[i] = -1;
+    if (lane == 0) kv_cnt[row] = k_keep;
   }
 }
 
-}  // namespace
-
-size_t mask_build_lds_bytes(int n_b, int d) {
-  const int n_pad = next_pow2(n_b);
-  const int rows = mask_rows_per_wg(n_pad);
-  size_t off = sizeof(uint64_t) * static_cast<size_t>(rows) * n_pad;
-  off += sizeof(double) * rows * d;
-  off += (n_pad + 15) & ~15;
-  off += sizeof(int) * kMaskThreads;
-  return off;
+template <int D>
+void launch_mask_build(int E, dim3 grid, hipStream_t s, const double* qbar,
+                       const double* kbar, const uint8_t* prot_flag, int H, int n_b,
+                       int k_keep, double sc, int32_t* kv_idx, int32_t* kv_cnt,
+                       uint8_t* mask, float* scores) {
+#define SA_MASK_CASE(EV)                                                                 \
+  case EV:                                                                               \
+    hipLaunchKernelGGL((mask_build_kernel<D, EV>), grid, dim3(kMaskThreads), 0, s, qbar,  \
+                       kbar, prot_flag, H, n_b, k_keep, sc, kv_idx, kv_cnt, mask, scores);  \
+    break;
+  switch (E) {
+    SA_MASK_CASE(1)
+    SA_MASK_CASE(2)
+    SA_MASK_CASE(4)
+    SA_MASK_CASE(8)
+    SA_MASK_CASE(16)
+    SA_MASK_CASE(32)
+    default: break;
+  }
+#undef SA_MASK_CASE
 }
+
+inline int mask_rows_per_wg(int E) { return 4 * (E >= 8 ? 1 : 8 / E); }
+
+}  // namespace
 
 void launch_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
                              int32_t* prot_idx, uint8_t* prot_flag,
@@ -264,19 +300,16 @@ void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
       hipLaunchKernelGGL((block_pool_kernel<float, 64>), pgrid, dim3(256), 0, s, q, k,
                          qbar, kbar, L_v, block);
   }
-  const int n_pad = next_pow2(n_b);
-  const size_t lds = mask_build_lds_bytes(n_b, d);
-  const int rows = mask_rows_per_wg(n_pad);
-  const dim3 mgrid(ceil_div(n_b, rows), P);
+  const int n_pad = next_pow2(n_b) < 64 ? 64 : next_pow2(n_b);
+  const int E = n_pad / 64;
+  const dim3 mgrid(ceil_div(n_b, mask_rows_per_wg(E)), P);
   const double sc = static_cast<double>(scale);
   if (d == 128)
-    hipLaunchKernelGGL(mask_build_kernel<128>, mgrid, dim3(kMaskThreads), lds, s, qbar,
-                       kbar, prot_flag, H, n_b, n_pad, rows, k_keep, sc, kv_idx,
-                       kv_cnt, mask, scores);
+    launch_mask_build<128>(E, mgrid, s, qbar, kbar, prot_flag, H, n_b, k_keep, sc, kv_idx,
+                           kv_cnt, mask, scores);
   else
-    hipLaunchKernelGGL(mask_build_kernel<64>, mgrid, dim3(kMaskThreads), lds, s, qbar,
-                       kbar, prot_flag, H, n_b, n_pad, rows, k_keep, sc, kv_idx,
-                       kv_cnt, mask, scores);
+    launch_mask_build<64>(E, mgrid, s, qbar, kbar, prot_flag, H, n_b, k_keep, sc, kv_idx,
+                          kv_cnt, mask, scores);
 }
 
 }  // namespace sa
