@@ -9,8 +9,9 @@ and block-sparse flash attention -- the four C-ABI calls, on one stream.
 Printed (one JSON line): ``value`` = effective dense-equivalent TFLOP/s of
 the layer (4*B*H*L_v^2*d / layer time), ``ms_per_step`` = ms per layer, a
 per-call breakdown from HIP events, the roofline of the dominant kernel
-(block-sparse attention, bf16 MFMA), the speedup over the same kernel run
-with every list full, and the fp64 oracle timed on a bounded sample.
+(block-sparse attention, bf16 MFMA; against the published peak and against the
+sustained MFMA rate measured on the device), the speedup over the same kernel
+run with every list full, and the fp64 oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -45,6 +46,8 @@ def parse():
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
                    help="run one device-to-device copy of this many MiB before "
                         "timing (a known-size reference for HBM byte counters)")
+    p.add_argument("--no-mfma-probe", action="store_true",
+                   help="skip the sustained-MFMA throughput probe")
     p.add_argument("--sweep", default=None,
                    help="also run the density x protection sweep, one JSON "
                         "line per cell appended to this file")
@@ -272,6 +275,18 @@ def main():
                      "traffic_src": traffic_src,
                      "algorithmic_bytes": 4 * w.B * w.H * w.L_v * w.d * (2 if w.dtype == "bf16" else 4)},
     }
+    if not args.no_mfma_probe:
+        # The matrix cores' sustained rate on this device, with changing random
+        # bf16 operands (the attention kernel's case) and with zero operands:
+        # MFMA power, and with it the clock, depends on the operand bits.
+        from paper_2608_15522_amd.binding import sa_bench_mfma_peak
+        rnd_tf, rnd_ghz = sa_bench_mfma_peak(True)
+        zero_tf, zero_ghz = sa_bench_mfma_peak(False)
+        res["roofline"]["measured_peak"] = {
+            "probe": "v_mfma_f32_32x32x16_bf16, 4 chains/wave, 4096 waves",
+            "random_operands_tflops": round(rnd_tf, 1), "random_operands_ghz": round(rnd_ghz, 2),
+            "zero_operands_tflops": round(zero_tf, 1), "zero_operands_ghz": round(zero_ghz, 2),
+            "frac_of_random_operands": round(achieved / rnd_tf, 4)}
     if args.sweep:
         run_sweep(args.sweep, max(3, args.dense_steps), torch, sa, synth, LayerPlan)
     if not args.no_cpu_baseline:

@@ -185,3 +185,40 @@ def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
         float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), ws.numel(),
         _stream()))
     return o, lse
+
+
+# ---- measurement helper library (libsa_bench.so, include/sa_bench.h) --------
+BENCH_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                              "libsa_bench.so")
+BENCH_SIGNATURES = {
+    "sa_bench_mfma_peak": (_I, [_I, _I, _I, ctypes.POINTER(_F), ctypes.POINTER(_F)]),
+}
+_bench_handle = None
+
+
+def bench_lib():
+    """The loaded measurement helper library (raises if it is not built)."""
+    global _bench_handle
+    if _bench_handle is None:
+        if not os.path.exists(BENCH_LIB_PATH):
+            raise SaError(-1, f"{BENCH_LIB_PATH} is missing: build it with "
+                              "`python -m paper_2608_15522_amd.build`")
+        handle = ctypes.CDLL(BENCH_LIB_PATH)
+        for name, (res, args) in BENCH_SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _bench_handle = handle
+    return _bench_handle
+
+
+def sa_bench_mfma_peak(random_operands: bool = True, iters: int = 4096,
+                       reps: int = 3):
+    """Sustained bf16 MFMA throughput of the current device: (TFLOP/s, GHz),
+    best of `reps` runs."""
+    tf, ghz = _F(0.0), _F(0.0)
+    rc = bench_lib().sa_bench_mfma_peak(int(bool(random_operands)), int(iters), int(reps),
+                                        ctypes.byref(tf), ctypes.byref(ghz))
+    if rc != 0:
+        raise SaError(rc, "sa_bench_mfma_peak failed")
+    return float(tf.value), float(ghz.value)

@@ -101,21 +101,6 @@ __device__ __forceinline__ void lds_dma16(const char* sbase, uint32_t voff, uint
       : "memory", "m0");
 }
 
-// Instruction classes of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSgValu = 0x002, kSgMfma = 0x008, kSgDsRead = 0x100;
-#ifndef SA_SCHED_GROUPS
-#define SA_SCHED_GROUPS 0
-#endif
-#ifndef SA_SG_QK
-#define SA_SG_QK 6
-#endif
-#ifndef SA_SG_PV
-#define SA_SG_PV 2
-#endif
-constexpr bool kSchedGroups = SA_SCHED_GROUPS != 0;
-constexpr int kSgValuQK = SA_SG_QK;  // VALU instructions after each QK^T MFMA
-constexpr int kSgValuPV = SA_SG_PV;  // VALU instructions after each PV MFMA
-
 template <bool B>
 struct CopyFlag {
   static constexpr bool value = B;
@@ -411,26 +396,6 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     mx_cur = tile_max(sn0, sn1);
     sc0 = sn0;
     sc1 = sn1;
-    // Issue order: the QK^T MFMAs of S(t+1), each followed by a share of the
-    // VALU work that forms P(t), then the PV MFMAs, each preceded by its two
-    // transposing reads and followed by a share of the max of S(t+1).
-    if constexpr (kSchedGroups) {
-      __builtin_amdgcn_sched_group_barrier(kSgDsRead, 4, 0);
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kSgValu, kSgValuQK, 0);
-        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kSgValu, kSgValuQK, 0);
-        if (kc + 2 < KC) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
-      }
-#pragma unroll
-      for (int j = 0; j < 4 * DT; ++j) {
-        __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kSgValu, kSgValuPV, 0);
-      }
-    }
     wait_dma();
     __syncthreads();
   };

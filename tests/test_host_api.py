@@ -12,6 +12,7 @@ from paper_2608_15522_amd import binding
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "sa.h")
+BENCH_HEADER = os.path.join(ROOT, "include", "sa_bench.h")
 
 FAKE = 0x10000          # aligned stand-in pointer, never dereferenced
 MISALIGNED = 0x10001
@@ -20,8 +21,8 @@ pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIB_PATH),
                                 reason="libsa.so not built")
 
 
-def declared_symbols():
-    text = open(HEADER).read()
+def declared_symbols(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(sa_[a-z_]+)\s*\(", text)))
 
@@ -33,6 +34,19 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert sa.sa_version() == 100
+
+
+@pytest.mark.skipif(not os.path.exists(binding.BENCH_LIB_PATH),
+                    reason="libsa_bench.so not built")
+def test_bench_library_exports_and_rejects_bad_arguments():
+    names = declared_symbols(BENCH_HEADER)
+    assert set(names) == set(binding.BENCH_SIGNATURES), names
+    lib = binding.bench_lib()
+    tf, ghz = ctypes.c_float(), ctypes.c_float()
+    # rejected before any device call
+    assert lib.sa_bench_mfma_peak(1, 0, 1, ctypes.byref(tf), ctypes.byref(ghz)) == -1
+    assert lib.sa_bench_mfma_peak(1, 8, 0, ctypes.byref(tf), ctypes.byref(ghz)) == -1
+    assert lib.sa_bench_mfma_peak(1, 8, 1, None, ctypes.byref(ghz)) == -1
 
 
 def test_workspace_sizes():
