@@ -2,73 +2,34 @@
 // direction).
 //
 // a->v: s^v_i = 1/(H*L_a) * sum_h sum_j softmax_i(scale * q^a_j . k^v_i).
-//   K1 a2v_lse_partial : per (b,h, 1024-key chunk, 512-query slab) a 16-wave
-//                        workgroup; wave w owns 32 audio queries and computes
-//                        S^T = K^v Q^a^T tiles with bf16 MFMA, so a lane owns
-//                        one audio query and keeps a lane-local online
-//                        (max, sum) over its keys; partials go to workspace.
+//   K1 a2v_lse_partial : per (1024-key chunk, 512-query slab, b*h) one 8-wave
+//                        workgroup holding the slab's audio queries (64 per
+//                        wave) streams the chunk's video keys with
+//                        S^T = K^v Q^a^T, so a lane owns an audio query and
+//                        keeps a lane-local (max, sum); partials go to
+//                        workspace.
 //   K1b lse_combine    : fixed-order merge of the chunk partials (log2 units).
-//   K2 a2v_colmass     : per (b, 128 video keys, group of 4 heads) a 16-wave
-//                        workgroup; wave w owns 32 audio queries and computes
-//                        S = Q^a K^v^T so a lane owns one video key column and
-//                        sums exp2(S*c - lse) over its rows, heads and query
-//                        slabs; the 32 lane/wave partials per key are added
-//                        in a fixed order.  No atomics: every output element
-//                        has one writer, so results are reproducible.
-//   K2b a2v_finalize   : sum over head groups, divide by H*L_a, block sums.
+//   K2 a2v_colmass     : per (1024-key chunk, h, b) the workgroup streams the
+//                        chunk's video keys once per audio slab with
+//                        S = Q^a K^v^T, so a lane owns a video key column and
+//                        sums exp2(S*c - lse) over its query rows; the 16
+//                        lane partials of a key are added in a fixed order.
+//   K2b a2v_finalize   : sum over heads, divide by H*L_a, block sums.
 // v->a: s^a_j = 1/(H*L_v) * sum_h sum_i softmax_j(scale * q^v_i . k^a_j).
-//   K3 v2a_colmass     : per (b,h, 512 video queries); pass 1 with S^T gives
-//                        each video query its log-sum-exp (lane-local), pass 2
-//                        recomputes S and reduces the column mass of every
-//                        64-key audio tile across the workgroup.
+//   K3 v2a_colmass     : per (512 video queries, 512-key audio window, b*h);
+//                        pass 1 streams every audio key with S^T for each
+//                        video query's log-sum-exp, pass 2 streams the window
+//                        with S and sums the column mass of each audio key.
 //   K3b v2a_chunk_sum  : fixed-order sum over video chunks per head, then
 //       v2a_finalize   : fixed-order sum over heads, / (H*L_v).
+// All bf16 kernels share one key-stream engine (below).  No atomics: every
+// output element has one writer, so results are reproducible.
 // fp32 inputs use plain per-thread kernels with the same outputs.
 #include "sa_device.h"
 #include "sa_internal.h"
 
 namespace sa {
 namespace {
-
-constexpr int kCT = 64;  // keys per LDS tile in K1/K3
-
-// Load a [64 x D] bf16 tile (rows >= row_end zero-filled) into swizzled LDS
-// with all threads of the workgroup.  Row r, 16-byte chunk cc lands at chunk
-// cc ^ (r & (CPR-1)).
-template <int D, int NT>
-__device__ __forceinline__ void load_rows_to_regs(const uint16_t* base, int row0,
-                                                  int row_end, u32x4* reg) {
-  constexpr int CPR = D / 8;
-  constexpr int CH = (kCT * CPR + NT - 1) / NT;
-#pragma unroll
-  for (int i = 0; i < CH; ++i) {
-    const int qq = threadIdx.x + NT * i;
-    const int row = qq / CPR, cc = qq % CPR;
-    reg[i] = (qq < kCT * CPR && row0 + row < row_end)
-                 ? ldg16(base + static_cast<size_t>(row0 + row) * D + cc * 8)
-                 : u32x4{0u, 0u, 0u, 0u};
-  }
-}
-template <int D, int NT>
-__device__ __forceinline__ void store_rows_to_lds(uint16_t* lds, const u32x4* reg) {
-  constexpr int CPR = D / 8;
-  constexpr int CH = (kCT * CPR + NT - 1) / NT;
-#pragma unroll
-  for (int i = 0; i < CH; ++i) {
-    const int qq = threadIdx.x + NT * i;
-    if (qq < kCT * CPR) {
-      const int row = qq / CPR, cc = qq % CPR;
-      stg16(lds + row * D + ((cc ^ (row & (CPR - 1))) * 8), reg[i]);
-    }
-  }
-}
-// Operand fragment of row `row` (of a swizzled [rows x D] LDS tile) for k-step kc.
-template <int D>
-__device__ __forceinline__ u32x4 lds_frag(const uint16_t* lds, int row, int kc, int g) {
-  constexpr int CPR = D / 8;
-  const int ch = 2 * kc + g;
-  return *reinterpret_cast<const u32x4*>(lds + row * D + ((ch ^ (row & (CPR - 1))) * 8));
-}
 
 template <int D>
 __device__ __forceinline__ void load_qfrag(const uint16_t* base, int row, int nrows,
@@ -79,76 +40,289 @@ __device__ __forceinline__ void load_qfrag(const uint16_t* base, int row, int nr
                          : u32x4{0u, 0u, 0u, 0u};
 }
 
+// ---- bf16 key-stream engine (K1, K2, K3) -------------------------------------
+// A workgroup of 8 waves holds 512 query rows in registers, 64 per wave as two
+// 32-row MFMA blocks, and streams 64-key tiles of one key matrix through an
+// LDS ring (plane layout of sa_device.h) in groups of two tiles: the copy of
+// the next group is in flight while the current one is read.  A wave works in units of 32 keys
+// (one half of a tile): the D/8 MFMAs of unit u+1 are interleaved with the
+// exponentials of unit u, so that the matrix cores and the vector ALU of a
+// SIMD work at the same time.
+constexpr int kXW = 8;                 // waves per workgroup
+constexpr int kXNT = kXW * 64;         // threads per workgroup
+constexpr int kGroup = 2;              // tiles per barrier interval
+constexpr int kRing = 2 * kGroup;      // stages of the LDS key ring
+static_assert(kXW * 64 == kQSlab && kXW * 64 == kV2aChunk,
+              "one workgroup holds one slab of 512 query rows");
+constexpr int kColKeys = 1024;         // video keys per K2 workgroup
+constexpr int kAWin = 512;             // audio keys per K3 column-mass window
+// A log-sum-exp unit whose sum against the running max reaches 2^64 is
+// redone against its own max (the running max is only raised then).
+constexpr float kSumGuard = 18446744073709551616.0f;
+
+template <int D>
+struct KeyRing {
+  static constexpr int TB = 128 * D;            // bytes per 64-key tile
+  static constexpr int CPT = TB / (16 * kXNT);  // 16-byte copies per thread per tile
+  static_assert(CPT >= 1 && CPT * 16 * kXNT == TB, "tile copy split");
+  uint32_t lds;         // LDS byte address of stage 0
+  uint32_t span[CPT];   // byte offset of this wave's 1 KB spans in a stage
+  int row[CPT];         // tile row copied by this lane
+  uint32_t col[CPT];    // byte offset of the lane's source slot within the row
+  int rd[2];            // lane offsets of the operand reads (k-step even / odd)
+
+  __device__ __forceinline__ void init(char* ring, int wave, int lane) {
+    lds = (uint32_t)(size_t)(lds_void_t*)ring;
+    const int n = lane & 31, g = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int sp = wave + kXW * i;  // span sp = plane sp/4, rows 16*(sp%4) ..
+      span[i] = sp * 1024;
+      row[i] = 16 * (sp & 3) + (lane >> 2);
+      col[i] = static_cast<uint32_t>((sp >> 2) * 64 + 16 * ((lane & 3) ^ plane_swz(row[i])));
+    }
+    // operand row n (+32 for the second unit of a tile), slot 2*(kc&1) + g
+    rd[0] = n * 64 + 16 * (g ^ plane_swz(n));
+    rd[1] = n * 64 + 16 * ((2 + g) ^ plane_swz(n));
+  }
+  // Copy keys [key0, key0 + 64) of the [L][D] matrix at src into stage st;
+  // rows past L repeat row L - 1.
+  __device__ __forceinline__ void issue(const char* src, int key0, int L, int st) const {
+    const char* base = src + static_cast<size_t>(key0) * (2 * D);
+    const int limit = min(63, L - 1 - key0);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      lds_dma16(base, static_cast<uint32_t>(min(row[i], limit) * (2 * D)) + col[i],
+                __builtin_amdgcn_readfirstlane(lds + st * TB + span[i]));
+  }
+};
+
+// MFMAs of one unit: keys 32*kb .. 32*kb+31 of the tile at `tile` against both
+// query blocks, into acc.  KEYS_A: acc[h] = K Q_h^T (a lane owns a query
+// column, its 16 elements are keys crow(i, g)); otherwise acc[h] = Q_h K^T (a
+// lane owns a key column, its elements are query rows 32h + crow(i, g)).
+// work(s), s = 0 .. D/8-1, runs on the vector ALU before the s-th MFMA.
+template <int D, bool KEYS_A, class W>
+__device__ __forceinline__ void unit_mfma(const char* tile, const int (&rd)[2], int kb,
+                                          const u32x4 (&qf)[2][D / 16], f32x16 (&acc)[2],
+                                          W&& work) {
+  constexpr int KC = D / 16;
+  auto rdk = [&](int kc) {
+    return *reinterpret_cast<const u32x4*>(tile + (kc >> 1) * 4096 + kb * 2048 + rd[kc & 1]);
+  };
+  u32x4 kf[KC];
+  kf[0] = rdk(0);
+  kf[1] = rdk(1);
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (kc + 2 < KC) kf[kc + 2] = rdk(kc + 2);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      work(2 * kc + h);
+      const f32x16 c0 = kc == 0 ? zero16() : acc[h];
+      acc[h] = KEYS_A ? mfma32x32x16(kf[kc], qf[h][kc], c0) : mfma32x32x16(qf[h][kc], kf[kc], c0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// Wait until at most n (0 <= n <= N, wave-uniform) vector-memory operations
+// of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm_le(int n) {
+  if constexpr (N > 0) {
+    if (n >= N) {
+      wait_vm<N>();
+      return;
+    }
+    wait_vm_le<N - 1>(n);
+  } else {
+    wait_vm<0>();
+  }
+}
+
+// Streams tiles t = 0 .. T-1 (T >= 1) of keys key_begin + 64t of the [L][D]
+// matrix at src; unit u = 2t + kb.  Tiles go through the ring in groups of
+// kGroup (stage t % kRing): the copies of group j+1 are issued right after
+// the barrier that opens group j, whose stages held group j-1, and are
+// awaited at the barrier that opens group j+1, so one barrier serves
+// 2*kGroup units of every wave.  acc.first(x) sees unit 0 once,
+// acc.slot(x, s, u, last) is the share of the work on a finished unit placed
+// beside the s-th MFMA of the next one, acc.fin(x, u, last) closes the unit;
+// `last` marks the units of tile T-1.  Ends with a barrier (ring free).
+template <int D, bool KEYS_A, class Acc>
+__device__ __forceinline__ void stream_keys(const KeyRing<D>& ring, const char* ring_lds,
+                                            const char* src, int key_begin, int L, int T,
+                                            const u32x4 (&qf)[2][D / 16], Acc& acc) {
+  constexpr int TB = KeyRing<D>::TB, CPT = KeyRing<D>::CPT, NS = D / 8;
+  auto issue_group = [&](int grp) {
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const int t = grp * kGroup + i;
+      if (t < T) ring.issue(src, key_begin + 64 * t, L, t % kRing);
+    }
+  };
+  issue_group(0);
+  issue_group(1);
+  // group 0 has landed once at most the copies of group 1 are outstanding
+  wait_vm_le<kGroup * CPT>(CPT * min(kGroup, max(0, T - kGroup)));
+  __syncthreads();
+  f32x16 a[2], b[2];
+  unit_mfma<D, KEYS_A>(ring_lds, ring.rd, 0, qf, a, [](int) {});
+  acc.first(a);
+  for (int t = 0; t + 1 < T; ++t) {
+    unit_mfma<D, KEYS_A>(ring_lds + (t % kRing) * TB, ring.rd, 1, qf, b,
+                         [&](int s) { acc.slot(a, s, 2 * t, false); });
+    acc.fin(a, 2 * t, false);
+    if ((t + 1) % kGroup == 0) {
+      wait_vm<0>();  // this wave's copies of the group that opens here
+      __syncthreads();
+      issue_group((t + 1) / kGroup + 1);
+    }
+    unit_mfma<D, KEYS_A>(ring_lds + ((t + 1) % kRing) * TB, ring.rd, 0, qf, a,
+                         [&](int s) { acc.slot(b, s, 2 * t + 1, false); });
+    acc.fin(b, 2 * t + 1, false);
+  }
+  unit_mfma<D, KEYS_A>(ring_lds + ((T - 1) % kRing) * TB, ring.rd, 1, qf, b,
+                       [&](int s) { acc.slot(a, s, 2 * T - 2, true); });
+  acc.fin(a, 2 * T - 2, true);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) acc.slot(b, s, 2 * T - 1, true);
+  acc.fin(b, 2 * T - 1, true);
+  __syncthreads();
+}
+
+// Lane-local online log2-sum-exp over the keys of KEYS_A units, for the two
+// query columns of the lane.  The running max m starts at the max of unit 0
+// and is raised only when a unit's sum against it reaches kSumGuard, so the
+// per-score work is one FMA, one exp2 and one add.  Keys >= key_end (tail of
+// the last tile) are masked to -inf.
+template <int D>
+struct LseAcc {
+  static constexpr int VPS = 32 / (D / 8);  // scores per lane per slot
+  float m[2], l[2], rs[2];
+  float c;
+  int key_begin, key_end, g;
+
+  __device__ __forceinline__ float val(const f32x16 (&x)[2], int h, int i, int u,
+                                       bool last) const {
+    const float v = x[h][i];
+    return (last && key_begin + 32 * u + crow(i, g) >= key_end) ? -INFINITY : v;
+  }
+  __device__ __forceinline__ void first(const f32x16 (&x)[2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float mx = x[h][0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) mx = fmaxf(mx, x[h][i]);
+      m[h] = mx * c;
+      l[h] = 0.f;
+    }
+  }
+  __device__ __forceinline__ void slot(const f32x16 (&x)[2], int s, int u, bool last) {
+#pragma unroll
+    for (int j = 0; j < VPS; ++j) {
+      const int v = s * VPS + j, h = v >> 4, i = v & 15;
+      const float p = fast_exp2(fmaf(val(x, h, i, u, last), c, -m[h]));
+      rs[h] = i == 0 ? p : rs[h] + p;
+    }
+    // keep this slot's share beside its MFMA (the compiler would otherwise
+    // sink it towards the first use of the sum)
+    asm volatile("" : "+v"(rs[(s * VPS) >> 4]));
+  }
+  __device__ __forceinline__ void fin(const f32x16 (&x)[2], int u, bool last) {
+    if (!(rs[0] < kSumGuard) || !(rs[1] < kSumGuard)) redo(x, u, last);
+    l[0] += rs[0];
+    l[1] += rs[1];
+  }
+  // Rare path: raise the running max to the unit's max and redo its sum.
+  __device__ __forceinline__ void redo(const f32x16 (&x)[2], int u, bool last) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (!(rs[h] < kSumGuard)) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, val(x, h, i, u, last));
+        const float mn = fmaxf(m[h], mx * c);
+        float r = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) r += fast_exp2(fmaf(val(x, h, i, u, last), c, -mn));
+        l[h] *= fast_exp2(m[h] - mn);
+        m[h] = mn;
+        rs[h] = r;
+      }
+    }
+  }
+  // (max, sum) of query column h over the keys of both lane halves.
+  __device__ __forceinline__ float2 merged(int h) const {
+    const float m2 = swap_halves(m[h]), l2 = swap_halves(l[h]);
+    const float mm = fmaxf(m[h], m2);
+    float lt = 0.f;
+    if (mm > -INFINITY) lt = l[h] * fast_exp2(m[h] - mm) + l2 * fast_exp2(m2 - mm);
+    return make_float2(mm, lt);
+  }
+};
+
+// Column mass of !KEYS_A units: the lane sums 2^(S*c - lse_row) over its 32
+// query rows and adds it to its own LDS slot of the unit's key (one writer
+// per slot, fixed order).  Rows without a query carry lse = +inf.
+template <int D>
+struct ColAcc {
+  static constexpr int VPS = 32 / (D / 8);
+  float lr[2][16];
+  float cs;
+  float c;
+  float* red;  // this lane's slot row, offset by its key column n
+
+  __device__ __forceinline__ void first(const f32x16 (&)[2]) {}
+  __device__ __forceinline__ void slot(const f32x16 (&x)[2], int s, int, bool) {
+#pragma unroll
+    for (int j = 0; j < VPS; ++j) {
+      const int v = s * VPS + j, h = v >> 4, i = v & 15;
+      const float p = fast_exp2(fmaf(x[h][i], c, -lr[h][i]));
+      cs = v == 0 ? p : cs + p;
+    }
+    asm volatile("" : "+v"(cs));
+  }
+  __device__ __forceinline__ void fin(const f32x16 (&)[2], int u, bool) { red[32 * u] += cs; }
+};
+
 // ---- K1 ---------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 a2v_lse_partial_kernel(const uint16_t* __restrict__ q_a,
                        const uint16_t* __restrict__ k_v,
                        float2* __restrict__ part, int L_v, int L_a, int nchunk,
                        float c) {
-  constexpr int NT = 1024, KC = D / 16;
-  constexpr int CH = (kCT * (D / 8) + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kCT * D];
+  __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
   const int chunk = blockIdx.x, slab = blockIdx.y, pair = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 5, n = lane & 31;
-  const int j = slab * kQSlab + wave * 32 + n;
-  const bool wave_on = slab * kQSlab + wave * 32 < L_a;
+  const int j0 = slab * kQSlab + wave * 64;  // first audio query row of the wave
   const int key_begin = chunk * kLseChunk;
   const int key_end = min(key_begin + kLseChunk, L_v);
-  const int ntiles = ceil_div(key_end - key_begin, kCT);
-  const uint16_t* kh = k_v + static_cast<size_t>(pair) * L_v * D;
 
-  u32x4 qf[KC];
-  load_qfrag<D>(q_a + static_cast<size_t>(pair) * L_a * D, j, L_a, g, qf);
-  float m = -INFINITY, l = 0.f;
-  u32x4 reg[CH];
-  load_rows_to_regs<D, NT>(kh, key_begin, key_end, reg);
-  store_rows_to_lds<D, NT>(Ks[0], reg);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int key0 = key_begin + t * kCT;
-    if (t + 1 < ntiles) load_rows_to_regs<D, NT>(kh, key0 + kCT, key_end, reg);
-    if (wave_on) {
-      f32x16 s0 = zero16(), s1 = zero16();
+  u32x4 qf[2][D / 16];
+  const uint16_t* qh = q_a + static_cast<size_t>(pair) * L_a * D;
+  load_qfrag<D>(qh, j0 + n, L_a, g, qf[0]);
+  load_qfrag<D>(qh, j0 + 32 + n, L_a, g, qf[1]);
+  KeyRing<D> ring;
+  ring.init(ring_lds, wave, lane);
+  LseAcc<D> acc;
+  acc.c = c;
+  acc.key_begin = key_begin;
+  acc.key_end = key_end;
+  acc.g = g;
+  stream_keys<D, true>(ring, ring_lds,
+                       reinterpret_cast<const char*>(k_v + static_cast<size_t>(pair) * L_v * D),
+                       key_begin, L_v, ceil_div(key_end - key_begin, 64), qf, acc);
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        s0 = mfma32x32x16(lds_frag<D>(Ks[buf], n, kc, g), qf[kc], s0);
-        s1 = mfma32x32x16(lds_frag<D>(Ks[buf], 32 + n, kc, g), qf[kc], s1);
-      }
-      if (key0 + kCT > key_end) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          if (key0 + crow(i, g) >= key_end) s0[i] = -INFINITY;
-          if (key0 + 32 + crow(i, g) >= key_end) s1[i] = -INFINITY;
-        }
-      }
-      float mx = s0[0];
-#pragma unroll
-      for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-      const float m_new = fmaxf(m, mx * c);
-      if (m_new > -INFINITY) {
-        float rs = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          rs += fast_exp2(fmaf(s0[i], c, -m_new)) + fast_exp2(fmaf(s1[i], c, -m_new));
-        l = fmaf(l, fast_exp2(m - m_new), rs);
-        m = m_new;
-      }
-    }
-    if (t + 1 < ntiles) store_rows_to_lds<D, NT>(Ks[buf ^ 1], reg);
-    __syncthreads();
+  for (int h = 0; h < 2; ++h) {
+    const float2 ml = acc.merged(h);
+    const int j = j0 + 32 * h + n;
+    if (g == 0 && j < L_a)
+      part[(static_cast<size_t>(pair) * nchunk + chunk) * L_a + j] = ml;
   }
-  // merge the two lanes that hold the same audio query
-  const float m2 = swap_halves(m), l2 = swap_halves(l);
-  const float mm = fmaxf(m, m2);
-  float lt = 0.f;
-  if (mm > -INFINITY) lt = l * fast_exp2(m - mm) + l2 * fast_exp2(m2 - mm);
-  if (g == 0 && j < L_a)
-    part[(static_cast<size_t>(pair) * nchunk + chunk) * L_a + j] = make_float2(mm, lt);
 }
 
 // lse2[pair][j] = log2(sum over chunks of l * 2^m), merged in chunk order.
@@ -170,202 +344,123 @@ __global__ void lse_combine_kernel(const float2* __restrict__ part,
 }
 
 // ---- K2 ---------------------------------------------------------------------
-// Column mass of one (batch, head) pair over a chunk of kColChunk video keys.
-// 8 waves; wave w owns audio queries 64*w .. 64*w+63 of the current 512-query
-// slab (two 32-row MFMA blocks), so every K operand read from LDS feeds two
-// MFMAs.  S = Q^a K^v^T puts one video key per lane column: the lane sums
-// exp2(S*c - lse) over its query rows and adds the result to its own slot of
-// an LDS partial array (one writer per slot, so the order is fixed); the 16
-// partials of a key (2 lane halves x 8 waves) are added in order at the end.
-// Query rows past L_a carry lse = +inf, so their probabilities are exactly 0;
-// keys past L_v only reach their own columns, which are not written.
-constexpr int kColChunk = 512;   // video keys per K2 workgroup
-constexpr int kColWaves = 8;     // 64 audio queries per wave
-
+// a->v column mass: grid (ceil(L_v/1024), H, B); the workgroup streams its
+// 1024 video keys once per slab of 512 audio queries (S = Q^a K^v^T, a lane
+// owns a key column) and adds exp2(S*c - lse) into per-lane LDS slots; the 16
+// slots of a key (8 waves x 2 lane halves) are then summed in a fixed order.
+// Keys past L_v only reach their own columns, which are not written.
 template <int D>
-__global__ void __launch_bounds__(kColWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
                    const uint16_t* __restrict__ k_v,
                    const float* __restrict__ lse2, float* __restrict__ colmass,
                    int H, int L_v, int L_a, float c) {
-  constexpr int NT = kColWaves * 64, KC = D / 16, CPR = D / 8;
-  constexpr int CH = (kCT * CPR + NT - 1) / NT;   // 16-byte chunks per thread per tile
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kCT * D];
-  __shared__ float red[kColWaves * 2][kColChunk];
+  constexpr int RS = kColKeys + 32;  // slot row stride (the two lane halves use different banks)
+  __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
+  __shared__ float red[2 * kXW][RS];
   const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 5, n = lane & 31;
-  const int key0 = chunk * kColChunk;
-  const int key_end = min(key0 + kColChunk, L_v);
+  const int key_begin = chunk * kColKeys;
+  const int key_end = min(key_begin + kColKeys, L_v);
   const size_t pair = static_cast<size_t>(b) * H + h;
-  const uint16_t* kh = k_v + pair * L_v * D;
   const uint16_t* qh = q_a + pair * L_a * D;
   const float* lh = lse2 + pair * L_a;
-  const int nslab = ceil_div(L_a, kQSlab);
-  const int ntiles = ceil_div(key_end - key0, kCT);
-  float* myred = red[2 * wave + g];
-  for (int i = n; i < kColChunk; i += 32) myred[i] = 0.f;
+  const char* kh = reinterpret_cast<const char*>(k_v + pair * L_v * D);
+  const int T = ceil_div(key_end - key_begin, 64);
 
-  for (int slab = 0; slab < nslab; ++slab) {
-    const int jb = slab * kQSlab + wave * 64;   // first query row of this wave
-    u32x4 qf[2][KC];
-    load_qfrag<D>(qh, jb + n, L_a, g, qf[0]);
-    load_qfrag<D>(qh, jb + 32 + n, L_a, g, qf[1]);
-    float lr[2][16];
+  KeyRing<D> ring;
+  ring.init(ring_lds, wave, lane);
+  ColAcc<D> acc;
+  acc.c = c;
+  acc.red = &red[2 * wave + g][n];
+  for (int k = 0; k < kColKeys; k += 32) acc.red[k] = 0.f;  // the lane's own slots
+
+  for (int slab = 0; slab * kQSlab < L_a; ++slab) {
+    const int j0 = slab * kQSlab + wave * 64;
+    u32x4 qf[2][D / 16];
+    load_qfrag<D>(qh, j0 + n, L_a, g, qf[0]);
+    load_qfrag<D>(qh, j0 + 32 + n, L_a, g, qf[1]);
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int jj = jb + 32 * qb + crow(i, g);
-        lr[qb][i] = jj < L_a ? lh[jj] : INFINITY;
+        const int jj = j0 + 32 * hh + crow(i, g);
+        acc.lr[hh][i] = jj < L_a ? lh[jj] : INFINITY;
       }
-    u32x4 reg[CH];
-    load_rows_to_regs<D, NT>(kh, key0, key_end, reg);
-    __syncthreads();  // the previous slab is done with both buffers
-    store_rows_to_lds<D, NT>(Ks[0], reg);
-    __syncthreads();
-#pragma unroll 1
-    for (int t = 0; t < ntiles; ++t) {
-      const int buf = t & 1;
-      if (t + 1 < ntiles) load_rows_to_regs<D, NT>(kh, key0 + (t + 1) * kCT, key_end, reg);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 s0 = zero16(), s1 = zero16();
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc) {
-          const u32x4 kf = lds_frag<D>(Ks[buf], 32 * kb + n, kc, g);
-          s0 = mfma32x32x16(qf[0][kc], kf, s0);
-          s1 = mfma32x32x16(qf[1][kc], kf, s1);
-        }
-        float cs = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          cs += fast_exp2(fmaf(s0[i], c, -lr[0][i])) + fast_exp2(fmaf(s1[i], c, -lr[1][i]));
-        myred[t * kCT + 32 * kb + n] += cs;
-      }
-      if (t + 1 < ntiles) store_rows_to_lds<D, NT>(Ks[buf ^ 1], reg);
-      __syncthreads();
-    }
+    stream_keys<D, false>(ring, ring_lds, kh, key_begin, L_v, T, qf, acc);
   }
-  __syncthreads();
-  for (int kk = threadIdx.x; kk < kColChunk; kk += NT) {
+  for (int k = threadIdx.x; k < kColKeys; k += kXNT) {
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < kColWaves * 2; ++w) sum += red[w][kk];
-    if (key0 + kk < L_v) colmass[pair * L_v + key0 + kk] = sum;
+    for (int w = 0; w < 2 * kXW; ++w) sum += red[w][k];
+    if (key_begin + k < L_v) colmass[pair * L_v + key_begin + k] = sum;
   }
 }
 
 // ---- K3 ---------------------------------------------------------------------
+// v->a column mass: grid (ceil(L_v/512), ceil(L_a/512), P).  The workgroup
+// holds 512 video queries; pass 1 streams every audio key with S^T = K^a
+// Q^v^T (a lane owns a video query) for its log2-sum-exp, pass 2 streams the
+// workgroup's window of 512 audio keys with S = Q^v K^a^T and sums the column
+// mass of each key over the 512 queries (per-lane LDS slots, fixed order).
 template <int D>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
                    const uint16_t* __restrict__ k_a, float* __restrict__ part,
                    int L_v, int L_a, int nchunk, float c) {
-  constexpr int NT = 1024, KC = D / 16;
-  constexpr int CH = (kCT * (D / 8) + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kCT * D];
-  __shared__ float lse_w[16][32];
-  __shared__ float red[16][2][kCT];
-  const int chunk = blockIdx.x, pair = blockIdx.y;
+  constexpr int RS = kAWin + 32;
+  __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
+  __shared__ float red[2 * kXW][RS];
+  __shared__ float lse_w[kXW][64];
+  const int chunk = blockIdx.x, win = blockIdx.y, pair = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 5, n = lane & 31;
-  const int ibase = chunk * kV2aChunk + wave * 32;
-  const bool wave_on = ibase < L_v;
-  const uint16_t* kah = k_a + static_cast<size_t>(pair) * L_a * D;
-  const int ntiles = ceil_div(L_a, kCT);
+  const int i0 = chunk * kV2aChunk + wave * 64;  // first video query row of the wave
+  const char* kah = reinterpret_cast<const char*>(k_a + static_cast<size_t>(pair) * L_a * D);
 
-  u32x4 qf[KC];
-  load_qfrag<D>(q_v + static_cast<size_t>(pair) * L_v * D, ibase + n, L_v, g, qf);
-  u32x4 reg[CH];
+  u32x4 qf[2][D / 16];
+  const uint16_t* qh = q_v + static_cast<size_t>(pair) * L_v * D;
+  load_qfrag<D>(qh, i0 + n, L_v, g, qf[0]);
+  load_qfrag<D>(qh, i0 + 32 + n, L_v, g, qf[1]);
+  KeyRing<D> ring;
+  ring.init(ring_lds, wave, lane);
 
-  // pass 1: log-sum-exp of every video query over all audio keys
-  float m = -INFINITY, l = 0.f;
-  load_rows_to_regs<D, NT>(kah, 0, L_a, reg);
-  store_rows_to_lds<D, NT>(Ks[0], reg);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int key0 = t * kCT;
-    if (t + 1 < ntiles) load_rows_to_regs<D, NT>(kah, key0 + kCT, L_a, reg);
-    if (wave_on) {
-      f32x16 s0 = zero16(), s1 = zero16();
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        s0 = mfma32x32x16(lds_frag<D>(Ks[buf], n, kc, g), qf[kc], s0);
-        s1 = mfma32x32x16(lds_frag<D>(Ks[buf], 32 + n, kc, g), qf[kc], s1);
-      }
-      if (key0 + kCT > L_a) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          if (key0 + crow(i, g) >= L_a) s0[i] = -INFINITY;
-          if (key0 + 32 + crow(i, g) >= L_a) s1[i] = -INFINITY;
-        }
-      }
-      float mx = s0[0];
-#pragma unroll
-      for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-      const float m_new = fmaxf(m, mx * c);
-      if (m_new > -INFINITY) {
-        float rs = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          rs += fast_exp2(fmaf(s0[i], c, -m_new)) + fast_exp2(fmaf(s1[i], c, -m_new));
-        l = fmaf(l, fast_exp2(m - m_new), rs);
-        m = m_new;
-      }
-    }
-    if (t + 1 < ntiles) store_rows_to_lds<D, NT>(Ks[buf ^ 1], reg);
-    __syncthreads();
-  }
+  // pass 1: log2-sum-exp of every video query over all audio keys
   {
-    const float m2 = swap_halves(m), l2 = swap_halves(l);
-    const float mm = fmaxf(m, m2);
-    float lt = 0.f;
-    if (mm > -INFINITY) lt = l * fast_exp2(m - mm) + l2 * fast_exp2(m2 - mm);
-    // rows past L_v get +inf: their probabilities are exactly 0
-    if (g == 0) lse_w[wave][n] = (ibase + n < L_v) ? mm + __log2f(lt) : INFINITY;
+    LseAcc<D> acc;
+    acc.c = c;
+    acc.key_begin = 0;
+    acc.key_end = L_a;
+    acc.g = g;
+    stream_keys<D, true>(ring, ring_lds, kah, 0, L_a, ceil_div(L_a, 64), qf, acc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float2 ml = acc.merged(h);
+      // rows past L_v get +inf: their probabilities are exactly 0
+      if (g == 0) lse_w[wave][32 * h + n] = (i0 + 32 * h + n < L_v) ? ml.x + __log2f(ml.y) : INFINITY;
+    }
   }
   __syncthreads();
-  float lr[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) lr[i] = lse_w[wave][crow(i, g)];
 
-  // pass 2: column mass of each 64-key audio tile
-  load_rows_to_regs<D, NT>(kah, 0, L_a, reg);
-  store_rows_to_lds<D, NT>(Ks[0], reg);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int key0 = t * kCT;
-    if (t + 1 < ntiles) load_rows_to_regs<D, NT>(kah, key0 + kCT, L_a, reg);
-    float cs0 = 0.f, cs1 = 0.f;
-    if (wave_on) {
-      f32x16 s0 = zero16(), s1 = zero16();
+  // pass 2: column mass of the window's audio keys
+  const int key_begin = win * kAWin;
+  const int key_end = min(key_begin + kAWin, L_a);
+  ColAcc<D> acc;
+  acc.c = c;
+  acc.red = &red[2 * wave + g][n];
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        s0 = mfma32x32x16(qf[kc], lds_frag<D>(Ks[buf], n, kc, g), s0);
-        s1 = mfma32x32x16(qf[kc], lds_frag<D>(Ks[buf], 32 + n, kc, g), s1);
-      }
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        cs0 += fast_exp2(fmaf(s0[i], c, -lr[i]));
-        cs1 += fast_exp2(fmaf(s1[i], c, -lr[i]));
-      }
-    }
-    red[wave][g][n] = cs0;
-    red[wave][g][32 + n] = cs1;
-    if (t + 1 < ntiles) store_rows_to_lds<D, NT>(Ks[buf ^ 1], reg);
-    __syncthreads();
-    if (threadIdx.x < kCT && key0 + static_cast<int>(threadIdx.x) < L_a) {
-      const int kk = threadIdx.x;
-      float sum = 0.f;
-      for (int w = 0; w < 16; ++w) sum += red[w][0][kk] + red[w][1][kk];
-      part[(static_cast<size_t>(pair) * nchunk + chunk) * L_a + key0 + kk] = sum;
-    }
-    __syncthreads();
+    for (int i = 0; i < 16; ++i) acc.lr[h][i] = lse_w[wave][32 * h + crow(i, g)];
+  for (int k = 0; k < kAWin; k += 32) acc.red[k] = 0.f;
+  stream_keys<D, false>(ring, ring_lds, kah, key_begin, L_a, ceil_div(key_end - key_begin, 64),
+                        qf, acc);
+  for (int k = threadIdx.x; k < key_end - key_begin; k += kXNT) {
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < 2 * kXW; ++w) sum += red[w][k];
+    part[(static_cast<size_t>(pair) * nchunk + chunk) * L_a + key_begin + k] = sum;
   }
 }
 
@@ -505,13 +600,13 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
   float2* lse_part = reinterpret_cast<float2*>(ws + lay.lse_part);
   float* lse_a = reinterpret_cast<float*>(ws + lay.lse_a);
   float* colmass = reinterpret_cast<float*>(ws + lay.colmass);
-  hipLaunchKernelGGL(a2v_lse_partial_kernel<D>, dim3(nchunk, nslab, P), dim3(1024), 0, s,
+  hipLaunchKernelGGL(a2v_lse_partial_kernel<D>, dim3(nchunk, nslab, P), dim3(kXNT), 0, s,
                      q_a, k_v, lse_part, L_v, L_a, nchunk, c);
   const size_t nlse = static_cast<size_t>(P) * L_a;
   hipLaunchKernelGGL(lse_combine_kernel, dim3((nlse + 255) / 256), dim3(256), 0, s,
                      lse_part, lse_a, P, L_a, nchunk);
-  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColChunk), H, B),
-                     dim3(kColWaves * 64), 0, s, q_a, k_v, lse_a, colmass, H, L_v, L_a, c);
+  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColKeys), H, B), dim3(kXNT),
+                     0, s, q_a, k_v, lse_a, colmass, H, L_v, L_a, c);
   const int n_b = ceil_div(L_v, block);
   hipLaunchKernelGGL(a2v_finalize_kernel, dim3(n_b, B), dim3(block), 0, s, colmass,
                      sal_v_tok, sal_v_blk, L_v, H,
@@ -520,8 +615,8 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
     float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
     float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
-    hipLaunchKernelGGL(v2a_colmass_kernel<D>, dim3(nchunk3, P), dim3(1024), 0, s, q_v,
-                       k_a, v2a_part, L_v, L_a, nchunk3, c);
+    hipLaunchKernelGGL(v2a_colmass_kernel<D>, dim3(nchunk3, ceil_div(L_a, kAWin), P),
+                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c);
     hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
                        v2a_part, v2a_head, L_a, nchunk3);
     const size_t na = static_cast<size_t>(B) * L_a;

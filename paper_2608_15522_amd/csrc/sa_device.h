@@ -65,6 +65,51 @@ __device__ __forceinline__ float fast_exp2(float x) {
   return __builtin_amdgcn_exp2f(x);
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// LDS tile layout: D/32 "planes" of [64 keys][32 d] bf16 (64 bytes per key
+// row, 4 KB per plane); 16-byte slot s of row r is stored at slot
+// s ^ plane_swz(r).  With this swizzle both the K operand reads
+// (ds_read_b128: 16 consecutive rows, one slot) and the transposing V reads
+// (ds_read_b64_tr_b16: 4 consecutive rows, two slots) are free of bank
+// conflicts, and every read address is a lane constant plus an immediate.
+__device__ __forceinline__ constexpr int plane_swz(int r) {
+  return ((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1);
+}
+
+// Copy of 16 bytes per lane, global -> LDS (global_load_lds_dwordx4): lane l
+// writes LDS bytes [lds_addr + 16*l, +16) with the 16 bytes at sbase + voff.
+// A 64-key tile of a [L][D] bf16 matrix is 4*D such chunks, i.e. 4*D/64 spans
+// of 1 KB; chunk i of the tile is LDS byte 16*i = plane i/256, row (i%256)/4,
+// physical slot i%4, holding logical slot (i%4) ^ plane_swz(row).
+//
+// The copy is issued with inline assembly on purpose: the compiler cannot
+// tell that an in-flight copy into one buffer does not alias the operand
+// reads of the other, and would otherwise wait for every copy (vmcnt(0))
+// before the first LDS read that follows it, serialising the pipeline.  The
+// kernel orders the buffers itself: s_waitcnt vmcnt(0) and a barrier end
+// every iteration, before any copied tile is read or a buffer is refilled.
+__device__ __forceinline__ void lds_dma16(const char* sbase, uint32_t voff, uint32_t lds_addr) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(sbase), "s"(lds_addr)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ void wait_dma() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+}
+// Wait until at most n (< 16) vector-memory operations of this wave are
+// outstanding; they complete in issue order.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
 __device__ __forceinline__ u32x4 ldg16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }

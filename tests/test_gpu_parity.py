@@ -31,6 +31,8 @@ SMALL = [
      BASE.with_(name="e", B=2, H=1, d=64, frames=3, rows=10, cols=13, L_a=520, n_plant=1), 1, 4),
     ("bf16_single_block",
      BASE.with_(name="f", H=1, frames=7, rows=11, cols=1, L_a=5, n_plant=0), 1, 0),
+    ("bf16_d128_La1100_three_slabs",
+     BASE.with_(name="h", H=2, frames=3, rows=10, cols=14, L_a=1100, n_plant=1), 2, 1),
     ("f32_d128_b128",
      synth.WORKLOADS["tiny_f32"].with_(name="g", d=128, block=128, frames=5, rows=10,
                                        cols=20, L_a=70, n_plant=2), 2, 1),
