@@ -43,17 +43,26 @@ inline CrossWs cross_ws_layout(int B, int H, int L_v, int L_a) {
   return w;
 }
 
+// Column count of the pooled block means and of the mask rows: the next
+// power of two >= n_b, at least 64.
+inline int mask_n_pad(int n_b) {
+  int p = 64;
+  while (p < n_b) p <<= 1;
+  return p;
+}
+
 struct MaskWs {
-  size_t qbar;   // double [B,H,n_b,d]
-  size_t kbar;   // double [B,H,n_b,d]
+  size_t qbar;   // double [B,H,d,n_pad]  pooled query means, block index innermost
+  size_t kbar;   // double [B,H,d,n_pad]  pooled key means, block index innermost
   size_t total;
 };
 
 inline MaskWs mask_ws_layout(int B, int H, int n_b, int d) {
   MaskWs w{};
+  const size_t n_pad = static_cast<size_t>(mask_n_pad(n_b));
   size_t off = 0;
-  w.qbar = off; off += align_up(sizeof(double) * B * H * n_b * d);
-  w.kbar = off; off += align_up(sizeof(double) * B * H * n_b * d);
+  w.qbar = off; off += align_up(sizeof(double) * B * H * d * n_pad);
+  w.kbar = off; off += align_up(sizeof(double) * B * H * d * n_pad);
   w.total = off;
   return w;
 }

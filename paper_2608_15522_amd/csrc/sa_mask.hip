@@ -4,13 +4,14 @@
 //    item one workgroup sorts the block saliencies in LDS with a bitonic
 //    network on 64-bit keys (value descending, index ascending) and takes
 //    the first k_prot.
-// K5 block_pool: per (b,h, block) the mean of Q and of K over the valid
-//    tokens of the block, accumulated in fp64 (16-byte loads, fixed-order LDS
-//    reduction); the sums of bf16/fp32 inputs are exact.
-// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and a group of query
-//    blocks, the pooled scores G = scale * qbar kbar^T by fp64 FMA (a few
-//    hundred MFLOP per layer; fp32 would misrank scores closer than ~1e-6,
-//    and pooled-score gaps are that small), then per row either the full list
+// K5 block_pool: per (b,h) and 8 consecutive blocks the mean of Q and of K
+//    over the valid tokens of each block, accumulated in fp64 (16-byte loads,
+//    fixed-order LDS reduction; the sums of bf16/fp32 inputs are exact),
+//    stored as [d][n_pad] (block index innermost).
+// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 16 query blocks,
+//    the pooled scores G = scale * qbar kbar^T by fp64 FMA (a few hundred
+//    MFLOP per layer; fp32 would misrank scores closer than ~1e-6, and
+//    pooled-score gaps are that small), then per row either the full list
 //    (protected row) or the top-k_keep blocks: one wave finds the k-th
 //    smallest order key (value descending, index ascending) by a bitwise
 //    search with ballots and compacts the blocks at or below it into an
@@ -66,140 +67,198 @@ template <> struct Elem<float> {
   }
 };
 
-// Grid (n_b, P), 256 threads.  out[pair][c][:] = mean of the rows of block c,
-// in fp64: the sums of bf16 or fp32 inputs are exact, the mean is rounded
-// once.
+constexpr int kMaxPoolBlock = 128;  // largest supported block
+
+// Grid (ceil(n_b / kPoolBlocks), P), 256 threads.  out[pair][:][c] (layout
+// [d][n_pad]) = mean of the rows of block c, in fp64: the sums of bf16 or
+// fp32 inputs are exact, the mean is rounded once.  Per block, thread
+// (rg, cc) loads 16-byte chunk cc of rows rg, rg + RG, ... of both matrices
+// (every load issued before the first sum) and the RG partial sums of each
+// element are added in a fixed order; the means of the workgroup's blocks
+// are written as runs of consecutive columns.
+constexpr int kPoolBlocks = 8;  // blocks per block_pool workgroup
+
 template <typename T, int D>
 __global__ void __launch_bounds__(256)
 block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
                   double* __restrict__ qbar, double* __restrict__ kbar, int L,
-                  int block) {
+                  int block, int n_b, int n_pad) {
   constexpr int EPC = Elem<T>::kPer16B;       // elements per 16-byte chunk
   constexpr int CPR = D / EPC;                // chunks per row
   constexpr int RG = 256 / CPR;               // row groups
-  __shared__ double part[RG][D];
-  const int c = blockIdx.x;
+  constexpr int NR = kMaxPoolBlock / RG;      // rows per thread, at most
+  __shared__ double part[2][RG][EPC][CPR];    // element e of chunk cc: consecutive cc
+  __shared__ double mean[2][D][kPoolBlocks];
+  const int c0 = blockIdx.x * kPoolBlocks;
   const size_t pair = blockIdx.y;
-  const int n_b = gridDim.x;
-  const int row0 = c * block;
-  const int len = min(block, L - row0);
+  const int nblk = min(kPoolBlocks, n_b - c0);
   const int cc = threadIdx.x % CPR, rg = threadIdx.x / CPR;
-  for (int which = 0; which < 2; ++which) {
-    const T* src = (which == 0 ? q : k) + pair * L * D;
-    double acc[EPC];
+  for (int j = 0; j < nblk; ++j) {
+    const int row0 = (c0 + j) * block;
+    const int len = min(block, L - row0);
+    u32x4 raw[2][NR];
 #pragma unroll
-    for (int e = 0; e < EPC; ++e) acc[e] = 0.0;
-    for (int r = rg; r < len; r += RG) {
-      double v[EPC];
-      Elem<T>::unpack(ldg16(src + static_cast<size_t>(row0 + r) * D + cc * EPC), v);
+    for (int which = 0; which < 2; ++which) {
+      const T* src = (which == 0 ? q : k) + pair * L * D;
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[e] += v[e];
+      for (int i = 0; i < NR; ++i) {
+        const int r = rg + RG * i;
+        raw[which][i] = r < len ? ldg16(src + static_cast<size_t>(row0 + r) * D + cc * EPC)
+                                : u32x4{0u, 0u, 0u, 0u};
+      }
     }
+    __syncthreads();  // the previous block's partial sums have been read
 #pragma unroll
-    for (int e = 0; e < EPC; ++e) part[rg][cc * EPC + e] = acc[e];
+    for (int which = 0; which < 2; ++which) {
+      double acc[EPC];
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[e] = 0.0;
+#pragma unroll
+      for (int i = 0; i < NR; ++i) {
+        if (rg + RG * i >= len) break;
+        double v[EPC];
+        Elem<T>::unpack(raw[which][i], v);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[e] += v[e];
+      }
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) part[which][rg][e][cc] = acc[e];
+    }
     __syncthreads();
-    if (threadIdx.x < D) {
+    for (int t = threadIdx.x; t < 2 * D; t += 256) {
+      const int which = t / D, dd = t % D;
       double sum = 0.0;
-      for (int i = 0; i < RG; ++i) sum += part[i][threadIdx.x];
-      double* dst = (which == 0 ? qbar : kbar);
-      dst[(pair * n_b + c) * D + threadIdx.x] = sum / static_cast<double>(len);
+      for (int i = 0; i < RG; ++i) sum += part[which][i][dd % EPC][dd / EPC];
+      mean[which][dd][j] = sum / static_cast<double>(len);
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < 2 * D * kPoolBlocks; t += 256) {
+    const int j = t % kPoolBlocks, dd = (t / kPoolBlocks) % D, which = t / (kPoolBlocks * D);
+    if (j < nblk) {
+      double* dst = (which == 0 ? qbar : kbar);
+      dst[(pair * D + dd) * n_pad + c0 + j] = mean[which][dd][j];
+    }
   }
 }
 
 // ---- K6 ---------------------------------------------------------------------
-constexpr int kMaskThreads = 256;  // 4 waves
+constexpr int kMaskWaves = 4;
+constexpr int kMaskThreads = kMaskWaves * 64;
 
-// k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 keys held
-// by one wave (E per lane), all distinct: bits are fixed from the top, each
-// step counting the keys that share the fixed prefix and have a 0 next.
+// Query-block rows per mask workgroup: the row exchange holds rows x n_pad
+// doubles in at most 64 KB of LDS, and from n_pad = 512 on fewer rows keep
+// phase 1 within the register budget.
+__host__ __device__ constexpr int mask_rows_per_wg(int E) {
+  return E >= 32 ? 4 : (E >= 8 ? 8 : 16);
+}
+
+// k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 distinct
+// keys held by one wave (E per lane).  Bits are fixed from the top; each step
+// counts the keys that share the fixed prefix and have a 0 next.  The search
+// stops once a single key shares the prefix: then key <= (k-th smallest)
+// exactly when (key & fixed) <= prefix, which is what the caller tests.
 template <int E>
-__device__ __forceinline__ uint64_t wave_kth_smallest(const uint64_t* keys, int k) {
-  uint64_t prefix = 0;
-  int below = 0;
-  for (int bit = 63; bit >= 0; --bit) {
-    const uint64_t hi = ~((2ull << bit) - 1ull);  // bits above `bit`
-    const uint64_t sel = hi | (1ull << bit);
+__device__ __forceinline__ void wave_kth_prefix(const uint64_t* keys, int k, uint64_t& prefix,
+                                                uint64_t& fixed) {
+  prefix = 0;
+  fixed = 0;
+  int below = 0, size = 64 * E;  // keys below the prefix / sharing it
+  for (int bit = 63; bit >= 0 && size > 1; --bit) {
+    const uint64_t sel = fixed | (1ull << bit);
     int cnt = 0;
 #pragma unroll
     for (int e = 0; e < E; ++e) cnt += __popcll(__ballot((keys[e] & sel) == prefix));
     if (below + cnt < k) {
       below += cnt;
+      size -= cnt;
       prefix |= 1ull << bit;
+    } else {
+      size = cnt;
     }
+    fixed = sel;
   }
-  return prefix;
 }
 
-// Grid (ceil(n_b / ROWS), P), 256 threads; template E = n_pad / 64 (n_pad the
-// next power of two >= n_b, at least 64).  Column col = 64*e + lane of a row
-// lives in register e of lane `lane`.  Each wave owns RW rows.
+// 1-D grid of 8 * ceil(P / 8) * ceil(n_b / R) workgroups, 4 waves; template
+// E = n_pad / 64.  Workgroup w runs on XCD w % 8 (round-robin dispatch) and
+// takes (b,h) pair (w % 8) + 8 * ((w / 8) / nrt) and row tile (w / 8) % nrt,
+// so all tiles of a pair share one XCD's L2 (workgroups past P exit).
+// Pooled means are [d][n_pad] per (b,h).  Phase 1: the workgroup's R query
+// rows are copied to LDS as [d][R]; wave w computes G = scale * qbar kbar^T
+// for them and the 64-column groups w, w+4, ... with one column per lane: the
+// lane's key values are loaded KP d-steps ahead into registers and each feeds
+// R fp64 FMAs whose query operands are LDS reads shared by the whole wave.
+// Rows >= n_b and columns >= n_b read padding and are discarded.  Phase 2:
+// the rows go through LDS; wave w takes rows w, w+4, ... with column
+// col = 64*e + lane in register e of lane `lane`, and either emits the full
+// list (protected row) or the top-k_keep blocks.
 template <int D, int E>
 __global__ void __launch_bounds__(kMaskThreads)
 mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kbar,
                   const uint8_t* __restrict__ prot_flag, int H, int n_b, int k_keep,
                   double scale, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt,
-                  uint8_t* __restrict__ mask, float* __restrict__ scores) {
+                  uint8_t* __restrict__ mask, float* __restrict__ scores, int P) {
   constexpr int NPAD = 64 * E;
-  constexpr int RW = E >= 8 ? 1 : 8 / E;          // rows per wave
-  constexpr int ROWS = 4 * RW;                     // rows per workgroup
-  constexpr int DCH = (8192 / NPAD) < D ? (8192 / NPAD) : D;  // d values per 64 KB stage
-  constexpr int KSS = NPAD + 1;                    // padded row: conflict-free stores
-  constexpr int PER = DCH * NPAD / kMaskThreads;   // staged values per thread
-  __shared__ double ks[DCH * KSS];
-  __shared__ double qs[ROWS * D];
+  constexpr int R = mask_rows_per_wg(E);
+  constexpr int KP = E >= 8 ? 16 : 32;  // d-steps of key values in flight per lane
+  constexpr int CUNR = E >= 8 ? 1 : 2;   // chunk pairs unrolled (register budget)
+  static_assert(D % (2 * KP) == 0 && R % 2 == 0, "chunking");
+  __shared__ double gs[R][NPAD];
+  __shared__ __attribute__((aligned(16))) double qs[D][R];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t pair = blockIdx.y;
-  const int b = static_cast<int>(pair / H);
-  const int r0 = blockIdx.x * ROWS;
-  const double* qb = qbar + pair * n_b * D;
-  const double* kb = kbar + pair * n_b * D;
+  const int nrt = ceil_div(n_b, R);
+  const int wg = blockIdx.x;
+  const int pair_i = (wg % 8) + 8 * ((wg / 8) / nrt);
+  if (pair_i >= P) return;  // uniform: the whole workgroup exits
+  const size_t pair = static_cast<size_t>(pair_i);
+  const int b = pair_i / H;
+  const int r0 = ((wg / 8) % nrt) * R;
+  const double* qp = qbar + pair * D * NPAD + r0;
+  const double* kp = kbar + pair * D * NPAD;
 
-  for (int i = tid; i < ROWS * D; i += kMaskThreads) {
-    const int rr = i / D;
-    qs[i] = r0 + rr < n_b ? qb[static_cast<size_t>(r0) * D + i] : 0.0;
-  }
-  double acc[RW][E];
+  for (int i = tid; i < D * R; i += kMaskThreads) qs[i / R][i % R] = qp[(i / R) * NPAD + i % R];
+  __syncthreads();
+#pragma unroll 1
+  for (int cg = wave; cg < E; cg += kMaskWaves) {
+    const int col = 64 * cg + lane;
+    double acc[R];
 #pragma unroll
-  for (int rr = 0; rr < RW; ++rr)
+    for (int i = 0; i < R; ++i) acc[i] = 0.0;
+    // key values of chunk c (KP d-steps) alternate between ka and kb
+    auto load_chunk = [&](double* kv, int c) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[rr][e] = 0.0;
-  for (int d0 = 0; d0 < D; d0 += DCH) {
-    // kbar[col][d0 .. d0+DCH) -> ks[dd][col]: every load of the stage is
-    // issued before the first store (DCH consecutive threads read one row)
-    double v[PER];
+      for (int j = 0; j < KP; ++j) kv[j] = kp[static_cast<size_t>(c * KP + j) * NPAD + col];
+    };
+    auto use_chunk = [&](const double* kv, int c) {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int i = tid + kMaskThreads * j;
-      const int col = i / DCH, dd = i % DCH;
-      v[j] = col < n_b ? kb[static_cast<size_t>(col) * D + d0 + dd] : 0.0;
-    }
-    __syncthreads();  // the previous stage has been consumed
+      for (int j = 0; j < KP; ++j) {
+        const double* qrow = qs[c * KP + j];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int i = tid + kMaskThreads * j;
-      ks[(i % DCH) * KSS + i / DCH] = v[j];
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int dd = 0; dd < DCH; ++dd) {
-      double kv[E];
-#pragma unroll
-      for (int e = 0; e < E; ++e) kv[e] = ks[dd * KSS + 64 * e + lane];
-#pragma unroll
-      for (int rr = 0; rr < RW; ++rr) {
-        const double qv = qs[(wave * RW + rr) * D + d0 + dd];
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[rr][e] = fma(qv, kv[e], acc[rr][e]);
+        for (int i = 0; i < R; i += 2) {
+          const double2 qq = *reinterpret_cast<const double2*>(qrow + i);
+          acc[i] = fma(qq.x, kv[j], acc[i]);
+          acc[i + 1] = fma(qq.y, kv[j], acc[i + 1]);
+        }
       }
+    };
+    double ka[KP], kb[KP];
+    load_chunk(ka, 0);
+#pragma unroll CUNR
+    for (int c = 0; c < D / KP; c += 2) {
+      load_chunk(kb, c + 1);
+      use_chunk(ka, c);
+      if (c + 2 < D / KP) load_chunk(ka, c + 2);
+      use_chunk(kb, c + 1);
     }
+#pragma unroll
+    for (int i = 0; i < R; ++i) gs[i][col] = acc[i] * scale;
   }
+  __syncthreads();
 
   const uint64_t below_mask = (1ull << lane) - 1ull;
-#pragma unroll
-  for (int rr = 0; rr < RW; ++rr) {
-    const int r = r0 + wave * RW + rr;
+  for (int i = wave; i < R; i += kMaskWaves) {
+    const int r = r0 + i;
     if (r >= n_b) break;  // uniform across the wave
     const size_t row = pair * n_b + r;
     int32_t* out_idx = kv_idx + row * n_b;
@@ -207,7 +266,7 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int col = 64 * e + lane;
-      const double gval = acc[rr][e] * scale;
+      const double gval = gs[i][col];
       keys[e] = col < n_b ? desc_double_asc_index_key(gval, static_cast<uint32_t>(col)) : ~0ull;
       if (scores != nullptr && col < n_b) scores[row * n_b + col] = static_cast<float>(gval);
     }
@@ -220,31 +279,34 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
       if (lane == 0) kv_cnt[row] = n_b;
       continue;
     }
-    const uint64_t kth = wave_kth_smallest<E>(keys, k_keep);
+    uint64_t prefix, fixed;
+    wave_kth_prefix<E>(keys, k_keep, prefix, fixed);
     int base = 0;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int col = 64 * e + lane;
-      const bool on = keys[e] <= kth;  // padding keys (~0) are never at or below it
+      // padding keys (~0) never pass: the k-th key is a real one
+      const bool on = (keys[e] & fixed) <= prefix;
       const uint64_t m = __ballot(on);
       if (on) out_idx[base + __popcll(m & below_mask)] = col;
       base += __popcll(m);
       if (mask != nullptr && col < n_b) mask[row * n_b + col] = on ? 1 : 0;
     }
-    for (int i = k_keep + lane; i < n_b; i += 64) out_idx[i] = -1;
+    for (int j = k_keep + lane; j < n_b; j += 64) out_idx[j] = -1;
     if (lane == 0) kv_cnt[row] = k_keep;
   }
 }
 
 template <int D>
 void launch_mask_build(int E, dim3 grid, hipStream_t s, const double* qbar,
-                       const double* kbar, const uint8_t* prot_flag, int H, int n_b,
+                       const double* kbar, const uint8_t* prot_flag, int P, int H, int n_b,
                        int k_keep, double sc, int32_t* kv_idx, int32_t* kv_cnt,
                        uint8_t* mask, float* scores) {
 #define SA_MASK_CASE(EV)                                                                 \
   case EV:                                                                               \
     hipLaunchKernelGGL((mask_build_kernel<D, EV>), grid, dim3(kMaskThreads), 0, s, qbar,  \
-                       kbar, prot_flag, H, n_b, k_keep, sc, kv_idx, kv_cnt, mask, scores);  \
+                       kbar, prot_flag, H, n_b, k_keep, sc, kv_idx, kv_cnt, mask, scores, \
+                       P);                                                                \
     break;
   switch (E) {
     SA_MASK_CASE(1)
@@ -258,7 +320,6 @@ void launch_mask_build(int E, dim3 grid, hipStream_t s, const double* qbar,
 #undef SA_MASK_CASE
 }
 
-inline int mask_rows_per_wg(int E) { return 4 * (E >= 8 ? 1 : 8 / E); }
 
 }  // namespace
 
@@ -280,35 +341,35 @@ void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
   const MaskWs lay = mask_ws_layout(B, H, n_b, d);
   double* qbar = reinterpret_cast<double*>(ws + lay.qbar);
   double* kbar = reinterpret_cast<double*>(ws + lay.kbar);
-  const dim3 pgrid(n_b, P);
+  const int n_pad = mask_n_pad(n_b);
+  const dim3 pgrid(ceil_div(n_b, kPoolBlocks), P);
   if (dtype == 0) {
     const uint16_t* q = static_cast<const uint16_t*>(q_v);
     const uint16_t* k = static_cast<const uint16_t*>(k_v);
     if (d == 128)
       hipLaunchKernelGGL((block_pool_kernel<uint16_t, 128>), pgrid, dim3(256), 0, s, q, k,
-                         qbar, kbar, L_v, block);
+                         qbar, kbar, L_v, block, n_b, n_pad);
     else
       hipLaunchKernelGGL((block_pool_kernel<uint16_t, 64>), pgrid, dim3(256), 0, s, q, k,
-                         qbar, kbar, L_v, block);
+                         qbar, kbar, L_v, block, n_b, n_pad);
   } else {
     const float* q = static_cast<const float*>(q_v);
     const float* k = static_cast<const float*>(k_v);
     if (d == 128)
       hipLaunchKernelGGL((block_pool_kernel<float, 128>), pgrid, dim3(256), 0, s, q, k,
-                         qbar, kbar, L_v, block);
+                         qbar, kbar, L_v, block, n_b, n_pad);
     else
       hipLaunchKernelGGL((block_pool_kernel<float, 64>), pgrid, dim3(256), 0, s, q, k,
-                         qbar, kbar, L_v, block);
+                         qbar, kbar, L_v, block, n_b, n_pad);
   }
-  const int n_pad = next_pow2(n_b) < 64 ? 64 : next_pow2(n_b);
   const int E = n_pad / 64;
-  const dim3 mgrid(ceil_div(n_b, mask_rows_per_wg(E)), P);
+  const dim3 mgrid(8 * ceil_div(P, 8) * ceil_div(n_b, mask_rows_per_wg(E)));
   const double sc = static_cast<double>(scale);
   if (d == 128)
-    launch_mask_build<128>(E, mgrid, s, qbar, kbar, prot_flag, H, n_b, k_keep, sc, kv_idx,
+    launch_mask_build<128>(E, mgrid, s, qbar, kbar, prot_flag, P, H, n_b, k_keep, sc, kv_idx,
                            kv_cnt, mask, scores);
   else
-    launch_mask_build<64>(E, mgrid, s, qbar, kbar, prot_flag, H, n_b, k_keep, sc, kv_idx,
+    launch_mask_build<64>(E, mgrid, s, qbar, kbar, prot_flag, P, H, n_b, k_keep, sc, kv_idx,
                           kv_cnt, mask, scores);
 }
 
