@@ -40,6 +40,23 @@ __device__ __forceinline__ void load_qfrag(const uint16_t* base, int row, int nr
                          : u32x4{0u, 0u, 0u, 0u};
 }
 
+// sum_{i < n} p[i * stride], added in index order; the loads are issued in
+// batches of 8 so that they are in flight together.
+__device__ __forceinline__ float sum_strided(const float* __restrict__ p, size_t stride,
+                                             int n) {
+  float acc = 0.f;
+  int i = 0;
+  for (; i + 8 <= n; i += 8) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = p[static_cast<size_t>(i + k) * stride];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc += v[k];
+  }
+  for (; i < n; ++i) acc += p[static_cast<size_t>(i) * stride];
+  return acc;
+}
+
 // ---- bf16 key-stream engine (K1, K2, K3) -------------------------------------
 // A workgroup of 8 waves holds 512 query rows in registers, 64 per wave as two
 // 32-row MFMA blocks, and streams 64-key tiles of one key matrix through an
@@ -325,20 +342,33 @@ a2v_lse_partial_kernel(const uint16_t* __restrict__ q_a,
   }
 }
 
-// lse2[pair][j] = log2(sum over chunks of l * 2^m), merged in chunk order.
-__global__ void lse_combine_kernel(const float2* __restrict__ part,
-                                   float* __restrict__ lse2, int P, int L_a,
-                                   int nchunk) {
+// lse2[pair][j] = log2(sum over chunks of l * 2^m), merged in chunk order
+// (max first, then the sum); one thread per (pair, j), loads in batches of 8.
+__global__ void __launch_bounds__(64)
+lse_combine_kernel(const float2* __restrict__ part, float* __restrict__ lse2, int P,
+                   int L_a, int nchunk) {
   const size_t t = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= static_cast<size_t>(P) * L_a) return;
   const size_t pair = t / L_a, j = t % L_a;
   const float2* p = part + pair * nchunk * L_a + j;
   float M = -INFINITY;
-  for (int ch = 0; ch < nchunk; ++ch) M = fmaxf(M, p[static_cast<size_t>(ch) * L_a].x);
+  for (int c0 = 0; c0 < nchunk; c0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      v[k] = c0 + k < nchunk ? p[static_cast<size_t>(c0 + k) * L_a].x : -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) M = fmaxf(M, v[k]);
+  }
   float S = 0.f;
-  for (int ch = 0; ch < nchunk; ++ch) {
-    const float2 v = p[static_cast<size_t>(ch) * L_a];
-    if (v.y > 0.f) S += v.y * fast_exp2(v.x - M);
+  for (int c0 = 0; c0 < nchunk; c0 += 8) {
+    float2 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      v[k] = c0 + k < nchunk ? p[static_cast<size_t>(c0 + k) * L_a] : make_float2(0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (v[k].y > 0.f) S += v[k].y * fast_exp2(v[k].x - M);
   }
   lse2[t] = M + __log2f(S);
 }
@@ -477,8 +507,7 @@ a2v_finalize_kernel(const float* __restrict__ colmass, float* __restrict__ sal_v
   const int i = c * blockDim.x + threadIdx.x;
   float v = 0.f;
   if (i < L_v) {
-    for (int gi = 0; gi < nsum; ++gi)
-      v += colmass[(static_cast<size_t>(b) * nsum + gi) * L_v + i];
+    v = sum_strided(colmass + static_cast<size_t>(b) * nsum * L_v + i, L_v, nsum);
     v *= inv_norm;
     if (sal_v_tok != nullptr) {
       float* dst = sal_v_tok + static_cast<size_t>(b) * L_v + i;
@@ -508,9 +537,9 @@ v2a_chunk_sum_kernel(const float* __restrict__ part, float* __restrict__ head_su
   const int ph = threadIdx.x >> 6;
   const size_t pair = blockIdx.y;
   float v = 0.f;
-  if (j < L_a)
-    for (int ch = ph; ch < nchunk; ch += 4)
-      v += part[(pair * nchunk + ch) * L_a + j];
+  if (j < L_a && ph < nchunk)
+    v = sum_strided(part + (pair * nchunk + ph) * L_a + j, 4 * static_cast<size_t>(L_a),
+                    (nchunk - ph + 3) / 4);
   red[ph][threadIdx.x & 63] = v;
   __syncthreads();
   if (ph == 0 && j < L_a)
@@ -526,9 +555,7 @@ __global__ void v2a_finalize_kernel(const float* __restrict__ part,
   const size_t t = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= static_cast<size_t>(B) * L_a) return;
   const size_t b = t / L_a, j = t % L_a;
-  float v = 0.f;
-  for (int p = 0; p < nparts; ++p)
-    v += part[(b * nparts + p) * L_a + j];
+  float v = sum_strided(part + b * nparts * L_a + j, L_a, nparts);
   v *= inv_norm;
   sal_a_tok[t] = accumulate ? sal_a_tok[t] + v : v;
 }
@@ -603,7 +630,7 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
   hipLaunchKernelGGL(a2v_lse_partial_kernel<D>, dim3(nchunk, nslab, P), dim3(kXNT), 0, s,
                      q_a, k_v, lse_part, L_v, L_a, nchunk, c);
   const size_t nlse = static_cast<size_t>(P) * L_a;
-  hipLaunchKernelGGL(lse_combine_kernel, dim3((nlse + 255) / 256), dim3(256), 0, s,
+  hipLaunchKernelGGL(lse_combine_kernel, dim3((nlse + 63) / 64), dim3(64), 0, s,
                      lse_part, lse_a, P, L_a, nchunk);
   hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColKeys), H, B), dim3(kXNT),
                      0, s, q_a, k_v, lse_a, colmass, H, L_v, L_a, c);
