@@ -16,7 +16,9 @@ Sparse Attention"):
   tie-break (lower index wins), at block granularity;
 * ``mask``       -- Eq. (6) and (9): the sparse pattern S_m as pooled-QK block
   top-k per query block, OR-ed with full rows for protected query blocks;
-* ``attention``  -- Eq. (5), (7), (10)/(11): dense and masked softmax attention.
+* ``attention``  -- Eq. (5), (7), (10)/(11): dense and masked softmax attention;
+* ``tokens``     -- Eq. (4) lagged saliency update, Eq. (8) at token level and
+  Eq. (11) with protected query tokens (dense rows over the block pattern).
 
 Where the paper is silent or ambiguous the reading taken is stated in the
 function that depends on it.  Parity status: every public function here is
@@ -29,11 +31,14 @@ from .mask import block_pool, pooled_scores, block_mask, kv_lists_from_mask
 from .attention import (dense_attention, masked_attention,
                         additive_mask_attention, key_tokens_of_row)
 from .layer import protected_sparse_layer, computed_flops, dense_flops
+from .tokens import (saliency_ema, select_protected_tokens,
+                     token_protected_attention, token_protected_rows)
 
 __all__ = [
     "cross_scores", "token_to_block_saliency", "topk_order",
     "select_protected", "block_pool", "pooled_scores", "block_mask",
     "kv_lists_from_mask", "dense_attention", "masked_attention",
     "additive_mask_attention", "key_tokens_of_row", "protected_sparse_layer",
-    "computed_flops", "dense_flops",
+    "computed_flops", "dense_flops", "saliency_ema", "select_protected_tokens",
+    "token_protected_attention", "token_protected_rows",
 ]
