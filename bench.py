@@ -12,6 +12,8 @@ per-call breakdown from HIP events, the roofline of the dominant kernel
 (block-sparse attention, bf16 MFMA; against the published peak and against the
 sustained MFMA rate measured on the device), the speedup over the same kernel
 run with every list full, and the fp64 oracle timed on a bounded sample.
+``token_protection`` reports the token-granular form of the protection on
+the same inputs (protected tokens instead of protected query blocks).
 """
 from __future__ import annotations
 
@@ -48,6 +50,11 @@ def parse():
                         "timing (a known-size reference for HBM byte counters)")
     p.add_argument("--no-mfma-probe", action="store_true",
                    help="skip the sustained-MFMA throughput probe")
+    p.add_argument("--token-rho", type=float, default=0.05,
+                   help="also time the token-granular protection (this fraction "
+                        "of the video tokens protected; 0 = skip)")
+    p.add_argument("--token-alpha", type=float, default=0.5,
+                   help="lagged-saliency weight alpha of Eq. (4) in that run")
     p.add_argument("--sweep", default=None,
                    help="also run the density x protection sweep, one JSON "
                         "line per cell appended to this file")
@@ -118,6 +125,55 @@ def time_layer(plan, t, steps, warmup, torch):
     per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
                 for j, n in enumerate(names)}
     return wall * 1e3 / steps, per_call
+
+
+def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
+    """The token-granular form of the protection on the same inputs, one
+    saliency-refresh step: cross-modal saliency, the lagged-cache update
+    (Eq. (4)), the protected tokens (Eq. (8) at token level), the block mask
+    without block protection, block-sparse attention, and the dense rows of
+    the protected tokens written over it (Eq. (11)).  Returns (ms per layer,
+    per-call ms, kv_cnt, kv_idx) of the last step."""
+    dev = t["q_v"].device
+    sal_bar = torch.zeros(w.B, w.L_v, dtype=torch.float32, device=dev)
+    tok_idx = torch.empty(w.B, k_tok, dtype=torch.int32, device=dev)
+    kv_idx = torch.empty_like(plan.kv_idx)
+    kv_cnt = torch.empty_like(plan.kv_cnt)
+    o = torch.empty_like(t["q_v"])
+    names = ["sa_cross_scores", "sa_saliency_ema", "sa_select_protected_tokens",
+             "sa_build_block_mask", "sa_sparse_attention", "sa_protected_token_attention"]
+
+    def step(e=None):
+        rec = (lambda j: e[j].record()) if e else (lambda j: None)
+        rec(0)
+        plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        rec(1)
+        sa.sa_saliency_ema(sal_bar, plan.sal_v_tok, alpha)
+        rec(2)
+        sa.sa_select_protected_tokens(sal_bar, k_tok, tok_idx=tok_idx, want_flag=False)
+        rec(3)
+        sa.sa_build_block_mask(t["q_v"], t["k_v"], plan.scale, plan.block, plan.k_keep,
+                               None, kv_idx=kv_idx, kv_cnt=kv_cnt, ws=plan.ws)
+        rec(4)
+        sa.sa_sparse_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, plan.block,
+                               kv_idx, kv_cnt, o=o, ws=plan.ws)
+        rec(5)
+        sa.sa_protected_token_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale,
+                                        tok_idx, o)
+        rec(6)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
+                for j, n in enumerate(names)}
+    return wall * 1e3 / steps, per_call, kv_idx.cpu().numpy(), kv_cnt.cpu().numpy()
 
 
 def time_attention(plan, t, kv_idx, kv_cnt, steps, torch, sa):
@@ -287,6 +343,24 @@ def main():
             "random_operands_tflops": round(rnd_tf, 1), "random_operands_ghz": round(rnd_ghz, 2),
             "zero_operands_tflops": round(zero_tf, 1), "zero_operands_ghz": round(zero_ghz, 2),
             "frac_of_random_operands": round(achieved / rnd_tf, 4)}
+    if args.token_rho > 0:
+        k_tok = synth.budget(args.token_rho, w.L_v)
+        ms_tok, pc_tok, kvi_tok, kvc_tok = time_token_layer(
+            plan, t, w, k_tok, args.token_alpha, args.steps, args.warmup, torch, sa)
+        rows_flops = 4.0 * w.d * k_tok * w.L_v * w.B * w.H
+        rows_ms = pc_tok["sa_protected_token_attention"]
+        rows_tf = rows_flops / (rows_ms * 1e-3) / 1e12
+        print(f"bench: token layer {ms_tok:.3f} ms {pc_tok}", file=sys.stderr, flush=True)
+        res["token_protection"] = {
+            "rho": args.token_rho, "k_tok": k_tok, "alpha": args.token_alpha,
+            "ms_per_layer": round(ms_tok, 4),
+            "value": round(dense_flops / (ms_tok * 1e-3) / 1e12, 3),
+            "per_call_ms": {k: round(v, 4) for k, v in pc_tok.items()},
+            "sparse_tflop": round(computed_flops(kvi_tok, kvc_tok, w.L_v, w.block, w.d) / 1e12, 4),
+            "dense_rows_tflop": round(rows_flops / 1e12, 4),
+            "dense_rows_kernel": "sparse_attn_bf16_kernel<128,128,gather>",
+            "dense_rows_tflops": round(rows_tf, 2),
+            "dense_rows_frac_of_peak": round(rows_tf / PEAK_BF16_TFLOPS, 4)}
     if args.sweep:
         run_sweep(args.sweep, max(3, args.dense_steps), torch, sa, synth, LayerPlan)
     if not args.no_cpu_baseline:

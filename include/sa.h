@@ -16,6 +16,12 @@
  *   4. sa_sparse_attention  -- block-sparse flash attention over the
  *                              compacted key-block lists (Sec. 4.2,
  *                              Eq. (10)/(11); Eq. (5) when every list is full).
+ * and the token-granular form of the protection:
+ *   5. sa_saliency_ema              -- lagged saliency cache update (Eq. (4));
+ *   6. sa_select_protected_tokens   -- protected query tokens by top-k of the
+ *                                      token saliency (Eq. (3)/(8));
+ *   7. sa_protected_token_attention -- dense rows of the protected tokens
+ *                                      over the sparse output (Eq. (9)-(11)).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -161,6 +167,61 @@ int sa_sparse_attention(const void* q, const void* k, const void* v, void* o,
                         float scale, int block, const int32_t* kv_idx,
                         const int32_t* kv_cnt, void* ws, size_t ws_bytes,
                         void* stream);
+
+/*
+ * sa_saliency_ema -- one update of the lagged saliency cache (Sec. 4.1,
+ * Eq. (4)): sal_bar[i] = alpha * sal_bar[i] + (1 - alpha) * sal[i] for
+ * i < n, in fp32.  The refresh schedule (every K denoising steps) is the
+ * caller's; Eq. (4) gives no alpha, so it is an argument.
+ *
+ *   sal_bar    [n] f32 in/out
+ *   sal        [n] f32 in; either the same buffer as sal_bar or disjoint
+ *   alpha      0 <= alpha <= 1
+ *   n          number of entries; 0 = nothing to do
+ */
+int sa_saliency_ema(float* sal_bar, const float* sal, size_t n, float alpha,
+                    void* stream);
+
+/*
+ * sa_select_protected_tokens -- protected query tokens (Sec. 4.2, Eq. (8);
+ * Sec. 4.1, Eq. (3)) at token granularity.
+ *
+ * Per batch item, the k_tok tokens of largest sal_tok (equal scores: lower
+ * token index first), listed in ascending token order.  The set is shared by
+ * all heads.
+ *
+ *   sal_tok    [B,L] f32 in (finite values), 1 <= L <= 262144
+ *   k_tok      0 <= k_tok <= L (the caller computes ceil(rho * L))
+ *   tok_idx    [B,k_tok] i32 out, ascending token order, nullable
+ *   tok_flag   [B,L] u8 out, 1 = protected, nullable
+ * At least one of tok_idx and tok_flag is non-NULL.  No workspace.
+ */
+int sa_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,
+                               int32_t* tok_idx, uint8_t* tok_flag,
+                               void* stream);
+
+/*
+ * sa_protected_token_attention -- dense attention rows of the protected
+ * query tokens (Sec. 4.2, Eq. (11) first case: Eq. (9) keeps every key of a
+ * protected query).
+ *
+ * For every head (b,h) and j < k_tok, token t = tok_idx[b,j] attends to all
+ * L keys with an exact softmax, and row t of o (and of lse) is overwritten.
+ * Run after sa_sparse_attention on lists built without block protection to
+ * obtain Eq. (11) with protected tokens; every other row is left as it is.
+ *
+ *   q, k, v    [B,H,L,d] in dtype; 1 <= L <= 262144
+ *   o          [B,H,L,d] in/out (round to nearest even from fp32)
+ *   lse        [B,H,L] f32 in/out, nullable
+ *   tok_idx    [B,k_tok] i32; entries outside [0,L) are skipped
+ *   k_tok      0 <= k_tok <= L; 0 = nothing to do
+ * No workspace.
+ */
+int sa_protected_token_attention(const void* q, const void* k, const void* v,
+                                 void* o, float* lse, int B, int H, int L,
+                                 int d, int dtype, float scale,
+                                 const int32_t* tok_idx, int k_tok,
+                                 void* stream);
 
 /*
  * Minimum workspace bytes of a call (SA_CALL_*) at the given sizes; L_a is

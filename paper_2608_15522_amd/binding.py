@@ -32,6 +32,10 @@ SIGNATURES = {
                                  _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "sa_sparse_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _F,
                                  _I, _VP, _VP, _VP, _SZ, _VP]),
+    "sa_saliency_ema": (_I, [_VP, _VP, _SZ, _F, _VP]),
+    "sa_select_protected_tokens": (_I, [_VP, _I, _I, _I, _VP, _VP, _VP]),
+    "sa_protected_token_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
+                                          _F, _VP, _I, _VP]),
     "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "sa_last_error": (ctypes.c_char_p, []),
     "sa_version": (_I, []),
@@ -184,6 +188,42 @@ def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
         float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), ws.numel(),
         _stream()))
+    return o, lse
+
+
+def sa_saliency_ema(sal_bar, sal, alpha):
+    """Lagged saliency update in place: sal_bar = alpha*sal_bar + (1-alpha)*sal."""
+    if sal_bar.dtype != torch.float32 or sal.dtype != torch.float32:
+        raise TypeError("saliency maps are float32")
+    if sal_bar.numel() != sal.numel():
+        raise ValueError("sal_bar and sal differ in size")
+    _check(lib().sa_saliency_ema(_ptr(sal_bar), _ptr(sal), sal_bar.numel(),
+                                 float(alpha), _stream()))
+    return sal_bar
+
+
+def sa_select_protected_tokens(sal_tok, k_tok, *, tok_idx=None, tok_flag=None,
+                               want_flag=True):
+    """Protected tokens; returns (tok_idx [B,k_tok] i32 ascending, tok_flag [B,L] u8)."""
+    B, L = sal_tok.shape
+    dev = sal_tok.device
+    if tok_idx is None:
+        tok_idx = torch.empty(B, max(k_tok, 0), dtype=torch.int32, device=dev)
+    if tok_flag is None and want_flag:
+        tok_flag = torch.empty(B, L, dtype=torch.uint8, device=dev)
+    _check(lib().sa_select_protected_tokens(_ptr(sal_tok), B, L, int(k_tok),
+                                            _ptr(tok_idx) if k_tok > 0 else None,
+                                            _ptr(tok_flag), _stream()))
+    return tok_idx, tok_flag
+
+
+def sa_protected_token_attention(q, k, v, scale, tok_idx, o, lse=None):
+    """Dense rows of the protected tokens written over o (and lse); returns (o, lse)."""
+    B, H, L, d = q.shape
+    k_tok = tok_idx.shape[1]
+    _check(lib().sa_protected_token_attention(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
+        float(scale), _ptr(tok_idx) if k_tok > 0 else None, int(k_tok), _stream()))
     return o, lse
 
 

@@ -223,4 +223,65 @@ int sa_sparse_attention(const void* q, const void* k, const void* v, void* o, fl
   return check_launch(fn);
 }
 
+int sa_saliency_ema(float* sal_bar, const float* sal, size_t n, float alpha, void* stream) {
+  const char* fn = "sa_saliency_ema";
+  if (!(alpha >= 0.f && alpha <= 1.f))
+    return fail(SA_ERR_INVALID_ARG, "%s: alpha=%g outside [0, 1]", fn,
+                static_cast<double>(alpha));
+  SA_TRY(check_tensor(fn, "sal_bar", sal_bar, true, 4));
+  SA_TRY(check_tensor(fn, "sal", sal, true, 4));
+  if (sal != sal_bar && sal < sal_bar + n && sal_bar < sal + n)
+    return fail(SA_ERR_INVALID_ARG, "%s: sal and sal_bar overlap without being equal", fn);
+  if (n == 0) return ok();
+  sa::launch_saliency_ema(sal_bar, sal, n, alpha, static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,
+                               int32_t* tok_idx, uint8_t* tok_flag, void* stream) {
+  const char* fn = "sa_select_protected_tokens";
+  if (B < 1 || L < 1) return fail(SA_ERR_INVALID_ARG, "%s: B=%d L=%d must be >= 1", fn, B, L);
+  if (L > sa::kMaxTokens)
+    return fail(SA_ERR_UNSUPPORTED, "%s: L=%d exceeds %d", fn, L, sa::kMaxTokens);
+  if (k_tok < 0 || k_tok > L)
+    return fail(SA_ERR_INVALID_ARG, "%s: k_tok=%d outside [0, L=%d]", fn, k_tok, L);
+  if (tok_idx == nullptr && tok_flag == nullptr)
+    return fail(SA_ERR_INVALID_ARG, "%s: tok_idx and tok_flag are both NULL", fn);
+  SA_TRY(check_tensor(fn, "sal_tok", sal_tok, true, 4));
+  SA_TRY(check_tensor(fn, "tok_idx", tok_idx, false, 4));
+  SA_TRY(check_tensor(fn, "tok_flag", tok_flag, false, 1));
+  sa::launch_select_protected_tokens(sal_tok, B, L, k_tok, tok_idx, tok_flag,
+                                     static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_protected_token_attention(const void* q, const void* k, const void* v, void* o,
+                                 float* lse, int B, int H, int L, int d, int dtype,
+                                 float scale, const int32_t* tok_idx, int k_tok,
+                                 void* stream) {
+  const char* fn = "sa_protected_token_attention";
+  SA_TRY(check_common(fn, B, H, L, d, dtype, scale, 128));
+  if (k_tok < 0 || k_tok > L)
+    return fail(SA_ERR_INVALID_ARG, "%s: k_tok=%d outside [0, L=%d]", fn, k_tok, L);
+  SA_TRY(check_tensor(fn, "q", q, true, 16));
+  SA_TRY(check_tensor(fn, "k", k, true, 16));
+  SA_TRY(check_tensor(fn, "v", v, true, 16));
+  SA_TRY(check_tensor(fn, "o", o, true, 16));
+  SA_TRY(check_tensor(fn, "lse", lse, false, 4));
+  SA_TRY(check_tensor(fn, "tok_idx", tok_idx, k_tok > 0, 4));
+  if (k_tok == 0) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == SA_BF16)
+    sa::launch_protected_token_attention_bf16(
+        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+        static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, B, H, L, d, scale,
+        tok_idx, k_tok, s);
+  else
+    sa::launch_protected_token_attention_f32(
+        static_cast<const float*>(q), static_cast<const float*>(k),
+        static_cast<const float*>(v), static_cast<float*>(o), lse, B, H, L, d, scale,
+        tok_idx, k_tok, s);
+  return check_launch(fn);
+}
+
 }  // extern "C"

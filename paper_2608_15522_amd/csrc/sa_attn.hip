@@ -81,7 +81,11 @@ __device__ __forceinline__ float max_halves(float x) {
   return fmaxf(x, fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1])));
 }
 
-template <int D, int BLOCK>
+// GATHER (dense rows of protected tokens, Eq. (11) first case): workgroup row
+// j of pair (b,h) is token rows[b*n_rows + j] (rows >= n_rows, or a token
+// outside [0, L), are skipped); every key tile is kept; O and lse are written
+// to the token's own row.  kv_idx, kv_cnt and order are not read.
+template <int D, int BLOCK, bool GATHER>
 __global__ void __launch_bounds__(BLOCK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         const uint16_t* __restrict__ k,
@@ -90,7 +94,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         const int32_t* __restrict__ kv_idx,
                         const int32_t* __restrict__ kv_cnt,
                         const int32_t* __restrict__ order, int P, int L,
-                        int n_b, float c) {
+                        int n_b, float c, const int32_t* __restrict__ rows, int n_rows,
+                        int H) {
   constexpr int NW = BLOCK / 32;             // waves per workgroup
   constexpr int TPB = BLOCK / kTile;         // tiles per key block
   constexpr int KC = D / 16;                 // k-steps of Q K^T
@@ -114,20 +119,28 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   // XCD x works through its pairs x, x+8, ... one at a time, heaviest query
   // block first: the K/V blocks of the pair in flight are shared through that
   // XCD's L2, and only 8 pairs are live at once across the chip.
+  const int n_q = GATHER ? ceil_div(n_rows, BLOCK) : n_b;  // query blocks per pair
   int pair, rank;
   if ((P & 7) == 0) {
     const int i = blockIdx.x >> 3;
-    pair = (blockIdx.x & 7) + 8 * (i / n_b);
-    rank = i % n_b;
+    pair = (blockIdx.x & 7) + 8 * (i / n_q);
+    rank = i % n_q;
   } else {
     pair = blockIdx.x % P;
     rank = blockIdx.x / P;
   }
   const size_t row_base = static_cast<size_t>(pair) * n_b;
-  const int r = order[row_base + rank];
-  int cnt = kv_cnt[row_base + r];
-  cnt = cnt < 0 ? 0 : (cnt > n_b ? n_b : cnt);
-  const int32_t* idx = kv_idx + (row_base + r) * n_b;
+  int r, cnt;
+  const int32_t* idx = nullptr;
+  if constexpr (GATHER) {
+    r = rank;
+    cnt = n_b;
+  } else {
+    r = order[row_base + rank];
+    cnt = kv_cnt[row_base + r];
+    cnt = cnt < 0 ? 0 : (cnt > n_b ? n_b : cnt);
+    idx = kv_idx + (row_base + r) * n_b;
+  }
 
   // Compact the list into 64-key tiles (wave 0): entries outside [0, n_b)
   // are dropped, and so is the second half of a last block of <= 64 keys.
@@ -139,7 +152,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     const uint64_t below = (1ull << lane) - 1ull;
     for (int i0 = 0; i0 < cnt; i0 += 64) {
       const int i = i0 + lane;
-      const int kb = i < cnt ? idx[i] : -1;
+      const int kb = i < cnt ? (GATHER ? i : idx[i]) : -1;
       const bool v0 = kb >= 0 && kb < n_b;
       const bool v1 = TPB == 2 && v0 && kb * BLOCK + kTile < L;
       const bool f0 = v0 && kb * BLOCK + kTile <= L;
@@ -163,12 +176,17 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   const char* kh = reinterpret_cast<const char*>(k + static_cast<size_t>(pair) * L * D);
   const char* vh = reinterpret_cast<const char*>(v + static_cast<size_t>(pair) * L * D);
 
-  const int qrow = r * BLOCK + (tid >> 6) * 32 + n;
+  int qrow = r * BLOCK + (tid >> 6) * 32 + n;
+  if constexpr (GATHER) {
+    qrow = qrow < n_rows ? rows[static_cast<size_t>(pair / H) * n_rows + qrow] : -1;
+    if (qrow >= L) qrow = -1;
+  }
+  const bool qvalid = GATHER ? qrow >= 0 : qrow < L;
   u32x4 qf[KC];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
-    qf[kc] = qrow < L ? ldg16(qh + static_cast<size_t>(qrow) * D + 16 * kc + 8 * g)
-                      : u32x4{0u, 0u, 0u, 0u};
+    qf[kc] = qvalid ? ldg16(qh + static_cast<size_t>(qrow) * D + 16 * kc + 8 * g)
+                    : u32x4{0u, 0u, 0u, 0u};
   }
 
   // DMA instruction i of wave w fills span w + NW*i of a tile: its lanes
@@ -498,7 +516,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 
   const float ltot = lsum + swap_halves(lsum);
   const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-  if (qrow < L) {
+  if (qvalid) {
     uint16_t* orow = o + (static_cast<size_t>(pair) * L + qrow) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -519,28 +537,40 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 // ---- fp32 path ------------------------------------------------------------
 constexpr int kF32Keys = 32;
 
-template <int D>
+// GATHER: as in the bf16 kernel, row j of pair (b,h) is token
+// rows[b*n_rows + j] and every key block is kept.
+template <int D, bool GATHER>
 __global__ void __launch_bounds__(128)
 sparse_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
                        const float* __restrict__ v, float* __restrict__ o,
                        float* __restrict__ lse,
                        const int32_t* __restrict__ kv_idx,
                        const int32_t* __restrict__ kv_cnt, int L, int n_b,
-                       int block, float scale) {
+                       int block, float scale, const int32_t* __restrict__ rows,
+                       int n_rows, int H) {
   __shared__ float Kt[kF32Keys][D + 1];
   __shared__ float Vt[kF32Keys][D];
   const int pair = blockIdx.y;
   const int r = blockIdx.x;
   const size_t row_base = static_cast<size_t>(pair) * n_b + r;
-  int cnt = kv_cnt[row_base];
-  cnt = cnt < 0 ? 0 : (cnt > n_b ? n_b : cnt);
-  const int32_t* idx = kv_idx + row_base * n_b;
+  int cnt = n_b;
+  const int32_t* idx = nullptr;
+  if constexpr (!GATHER) {
+    cnt = kv_cnt[row_base];
+    cnt = cnt < 0 ? 0 : (cnt > n_b ? n_b : cnt);
+    idx = kv_idx + row_base * n_b;
+  }
   const float* qh = q + static_cast<size_t>(pair) * L * D;
   const float* kh = k + static_cast<size_t>(pair) * L * D;
   const float* vh = v + static_cast<size_t>(pair) * L * D;
   const int tid = threadIdx.x;
-  const int qrow = r * block + tid;
-  const bool active = tid < block && qrow < L;
+  int qrow = r * block + tid;
+  bool active = tid < block && qrow < L;
+  if constexpr (GATHER) {
+    active = tid < block && qrow < n_rows;
+    qrow = active ? rows[static_cast<size_t>(pair / H) * n_rows + qrow] : -1;
+    active = active && qrow >= 0 && qrow < L;
+  }
 
   float qv[D], acc[D];
 #pragma unroll
@@ -551,7 +581,7 @@ sparse_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
   float m = -INFINITY, l = 0.f;
 
   for (int i = 0; i < cnt; ++i) {
-    const int kb = idx[i];
+    const int kb = GATHER ? i : idx[i];
     if (kb < 0 || kb >= n_b) continue;
     const int kend = min((kb + 1) * block, L);
     for (int key0 = kb * block; key0 < kend; key0 += kF32Keys) {
@@ -606,17 +636,17 @@ void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
   hipLaunchKernelGGL(order_rows_kernel, dim3(P), dim3(256), 0, s, kv_cnt, order, n_b);
   const dim3 grid(P * n_b);
   if (d == 128 && block == 128)
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 128>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 128, false>), grid, dim3(256), 0, s,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
   else if (d == 128 && block == 64)
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 64>), grid, dim3(128), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 64, false>), grid, dim3(128), 0, s,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
   else if (d == 64 && block == 128)
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 128>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 128, false>), grid, dim3(256), 0, s,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
   else
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 64>), grid, dim3(128), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c);
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 64, false>), grid, dim3(128), 0, s,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
 }
 
 void launch_sparse_attention_f32(const float* q, const float* k,
@@ -627,11 +657,48 @@ void launch_sparse_attention_f32(const float* q, const float* k,
   const int n_b = ceil_div(L, block);
   const dim3 grid(n_b, B * H);
   if (d == 128)
-    hipLaunchKernelGGL(sparse_attn_f32_kernel<128>, grid, dim3(128), 0, s, q, k, v,
-                       o, lse, kv_idx, kv_cnt, L, n_b, block, scale);
+    hipLaunchKernelGGL((sparse_attn_f32_kernel<128, false>), grid, dim3(128), 0, s, q, k, v,
+                       o, lse, kv_idx, kv_cnt, L, n_b, block, scale, nullptr, 0, H);
   else
-    hipLaunchKernelGGL(sparse_attn_f32_kernel<64>, grid, dim3(128), 0, s, q, k, v,
-                       o, lse, kv_idx, kv_cnt, L, n_b, block, scale);
+    hipLaunchKernelGGL((sparse_attn_f32_kernel<64, false>), grid, dim3(128), 0, s, q, k, v,
+                       o, lse, kv_idx, kv_cnt, L, n_b, block, scale, nullptr, 0, H);
+}
+
+// Dense rows of the protected tokens (Eq. (11) first case), written over O
+// and lse: the gather variants, blocks of 128 gathered rows, no workspace.
+void launch_protected_token_attention_bf16(const uint16_t* q, const uint16_t* k,
+                                           const uint16_t* v, uint16_t* o, float* lse,
+                                           int B, int H, int L, int d, float scale,
+                                           const int32_t* tok_idx, int k_tok,
+                                           hipStream_t s) {
+  constexpr int kRowBlock = 128;
+  const int n_b = ceil_div(L, kRowBlock);
+  const int P = B * H;
+  const float c = scale * kLog2e;
+  const dim3 grid(P * ceil_div(k_tok, kRowBlock));
+  if (d == 128)
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, kRowBlock, true>), grid, dim3(256), 0, s,
+                       q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
+                       k_tok, H);
+  else
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, kRowBlock, true>), grid, dim3(256), 0, s,
+                       q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
+                       k_tok, H);
+}
+
+void launch_protected_token_attention_f32(const float* q, const float* k, const float* v,
+                                          float* o, float* lse, int B, int H, int L, int d,
+                                          float scale, const int32_t* tok_idx, int k_tok,
+                                          hipStream_t s) {
+  constexpr int kRowBlock = 128;
+  const int n_b = ceil_div(L, kRowBlock);
+  const dim3 grid(ceil_div(k_tok, kRowBlock), B * H);
+  if (d == 128)
+    hipLaunchKernelGGL((sparse_attn_f32_kernel<128, true>), grid, dim3(128), 0, s, q, k, v,
+                       o, lse, nullptr, nullptr, L, n_b, kRowBlock, scale, tok_idx, k_tok, H);
+  else
+    hipLaunchKernelGGL((sparse_attn_f32_kernel<64, true>), grid, dim3(128), 0, s, q, k, v,
+                       o, lse, nullptr, nullptr, L, n_b, kRowBlock, scale, tok_idx, k_tok, H);
 }
 
 }  // namespace sa

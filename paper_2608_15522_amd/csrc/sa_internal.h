@@ -81,6 +81,20 @@ inline AttnWs attn_ws_layout(int B, int H, int n_b, int /*d*/, int /*block*/) {
 }
 
 // ---- launchers (defined in the kernel sources) ----------------------------
+constexpr int kMaxTokens = kMaxBlocks * 128;  // longest token sequence (L)
+void launch_saliency_ema(float* s_bar, const float* s, size_t n, float alpha,
+                         hipStream_t st);
+void launch_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,
+                                    int32_t* tok_idx, uint8_t* tok_flag, hipStream_t st);
+void launch_protected_token_attention_bf16(const uint16_t* q, const uint16_t* k,
+                                           const uint16_t* v, uint16_t* o, float* lse,
+                                           int B, int H, int L, int d, float scale,
+                                           const int32_t* tok_idx, int k_tok,
+                                           hipStream_t s);
+void launch_protected_token_attention_f32(const float* q, const float* k, const float* v,
+                                          float* o, float* lse, int B, int H, int L, int d,
+                                          float scale, const int32_t* tok_idx, int k_tok,
+                                          hipStream_t s);
 void launch_cross_scores_bf16(const uint16_t* q_a, const uint16_t* k_v,
                               const uint16_t* q_v, const uint16_t* k_a, int B,
                               int H, int L_v, int L_a, int d, float scale,

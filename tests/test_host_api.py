@@ -98,7 +98,46 @@ def _select(**kw):
     return sa.lib().sa_select_protected(*a.values())
 
 
+def _ema(**kw):
+    a = dict(sal_bar=FAKE, sal=FAKE, n=1000, alpha=0.5, stream=None)
+    a.update(kw)
+    return sa.lib().sa_saliency_ema(*a.values())
+
+
+def _tokens(**kw):
+    a = dict(sal_tok=FAKE, B=1, L=1000, k_tok=50, tok_idx=FAKE, tok_flag=None,
+             stream=None)
+    a.update(kw)
+    return sa.lib().sa_select_protected_tokens(*a.values())
+
+
+def _ptok(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
+             dtype=0, scale=0.088, tok_idx=FAKE, k_tok=10, stream=None)
+    a.update(kw)
+    return sa.lib().sa_protected_token_attention(*a.values())
+
+
 @pytest.mark.parametrize("call,kw,code,needle", [
+    (_ema, dict(alpha=1.5), sa.SA_ERR_INVALID_ARG, "alpha"),
+    (_ema, dict(alpha=float("nan")), sa.SA_ERR_INVALID_ARG, "alpha"),
+    (_ema, dict(sal_bar=None), sa.SA_ERR_INVALID_ARG, "sal_bar is NULL"),
+    (_ema, dict(sal=FAKE + 64), sa.SA_ERR_INVALID_ARG, "overlap"),
+    (_ema, dict(sal=MISALIGNED + 1), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_tokens, dict(k_tok=-1), sa.SA_ERR_INVALID_ARG, "k_tok"),
+    (_tokens, dict(k_tok=1001), sa.SA_ERR_INVALID_ARG, "k_tok"),
+    (_tokens, dict(L=0), sa.SA_ERR_INVALID_ARG, "L=0"),
+    (_tokens, dict(L=2048 * 128 + 1, k_tok=1), sa.SA_ERR_UNSUPPORTED, "exceeds"),
+    (_tokens, dict(tok_idx=None), sa.SA_ERR_INVALID_ARG, "both NULL"),
+    (_tokens, dict(sal_tok=None), sa.SA_ERR_INVALID_ARG, "sal_tok is NULL"),
+    (_tokens, dict(tok_flag=FAKE, tok_idx=MISALIGNED + 1), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_ptok, dict(k_tok=1001), sa.SA_ERR_INVALID_ARG, "k_tok"),
+    (_ptok, dict(k_tok=-1), sa.SA_ERR_INVALID_ARG, "k_tok"),
+    (_ptok, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
+    (_ptok, dict(L=2049 * 128), sa.SA_ERR_UNSUPPORTED, "n_b"),
+    (_ptok, dict(tok_idx=None), sa.SA_ERR_INVALID_ARG, "tok_idx is NULL"),
+    (_ptok, dict(o=None), sa.SA_ERR_INVALID_ARG, "o is NULL"),
+    (_ptok, dict(scale=-1.0), sa.SA_ERR_INVALID_ARG, "scale"),
     (_attn, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
     (_attn, dict(block=32), sa.SA_ERR_UNSUPPORTED, "block"),
     (_attn, dict(dtype=7), sa.SA_ERR_UNSUPPORTED, "dtype"),
@@ -141,6 +180,12 @@ def test_invalid_arguments_are_rejected(call, kw, code, needle):
     assert rc == code
     msg = sa.sa_last_error()
     assert needle in msg, msg
+
+
+def test_empty_token_calls_launch_nothing():
+    """k_tok = 0 and n = 0 are valid and return before any launch."""
+    assert _ptok(k_tok=0, tok_idx=None) == sa.SA_OK
+    assert _ema(n=0) == sa.SA_OK
 
 
 def test_binding_raises_without_gpu_tensors():
