@@ -18,7 +18,9 @@ Sparse Attention"):
   top-k per query block, OR-ed with full rows for protected query blocks;
 * ``attention``  -- Eq. (5), (7), (10)/(11): dense and masked softmax attention;
 * ``tokens``     -- Eq. (4) lagged saliency update, Eq. (8) at token level and
-  Eq. (11) with protected query tokens (dense rows over the block pattern).
+  Eq. (11) with protected query tokens (dense rows over the block pattern);
+* ``cache``      -- Eq. (12)-(15): the synchronization-aware cache-reuse
+  indicator (relative L1 changes, protected-row change, saliency drift).
 
 Where the paper is silent or ambiguous the reading taken is stated in the
 function that depends on it.  Parity status: every public function here is
@@ -33,6 +35,7 @@ from .attention import (dense_attention, masked_attention,
 from .layer import protected_sparse_layer, computed_flops, dense_flops
 from .tokens import (saliency_ema, select_protected_tokens,
                      token_protected_attention, token_protected_rows)
+from .cache import relative_l1, saliency_drift, cache_indicator
 
 __all__ = [
     "cross_scores", "token_to_block_saliency", "topk_order",
@@ -40,5 +43,6 @@ __all__ = [
     "kv_lists_from_mask", "dense_attention", "masked_attention",
     "additive_mask_attention", "key_tokens_of_row", "protected_sparse_layer",
     "computed_flops", "dense_flops", "saliency_ema", "select_protected_tokens",
-    "token_protected_attention", "token_protected_rows",
+    "token_protected_attention", "token_protected_rows", "relative_l1",
+    "saliency_drift", "cache_indicator",
 ]
