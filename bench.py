@@ -13,7 +13,9 @@ per-call breakdown from HIP events, the roofline of the dominant kernel
 sustained MFMA rate measured on the device), the speedup over the same kernel
 run with every list full, and the fp64 oracle timed on a bounded sample.
 ``token_protection`` reports the token-granular form of the protection on
-the same inputs (protected tokens instead of protected query blocks).
+the same inputs (protected tokens instead of protected query blocks), and
+``cache_indicator`` the cache-reuse indicator on block outputs of the same
+size (HBM-bound).
 """
 from __future__ import annotations
 
@@ -55,6 +57,8 @@ def parse():
                         "of the video tokens protected; 0 = skip)")
     p.add_argument("--token-alpha", type=float, default=0.5,
                    help="lagged-saliency weight alpha of Eq. (4) in that run")
+    p.add_argument("--no-cache-indicator", action="store_true",
+                   help="skip timing the cache-reuse indicator")
     p.add_argument("--sweep", default=None,
                    help="also run the density x protection sweep, one JSON "
                         "line per cell appended to this file")
@@ -174,6 +178,39 @@ def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
     per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
                 for j, n in enumerate(names)}
     return wall * 1e3 / steps, per_call, kv_idx.cpu().numpy(), kv_cnt.cpu().numpy()
+
+
+def time_cache_indicator(w, steps, torch, sa):
+    """The cache-reuse indicator (Eq. (12)-(15)) on block outputs of the
+    workload's size (C = H*d channels per token, its dtype): current and
+    cached video and audio outputs, 5 % protected token rows, both saliency
+    maps.  Returns (ms per call, algorithmic bytes)."""
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    C = w.H * w.d
+    g = torch.Generator(device="cuda").manual_seed(0)
+    yv = torch.randn(w.B, w.L_v, C, device="cuda", generator=g).to(dt)
+    yvh = torch.randn(w.B, w.L_v, C, device="cuda", generator=g).to(dt)
+    ya = torch.randn(w.B, w.L_a, C, device="cuda", generator=g).to(dt)
+    yah = torch.randn(w.B, w.L_a, C, device="cuda", generator=g).to(dt)
+    flag = (torch.rand(w.B, w.L_v, device="cuda", generator=g) < 0.05).to(torch.uint8)
+    sb = torch.rand(w.B, w.L_v, device="cuda", generator=g)
+    sh = torch.rand(w.B, w.L_v, device="cuda", generator=g)
+    out = torch.empty(6, dtype=torch.float32, device="cuda")
+    call = lambda: sa.sa_cache_indicator(yv, yvh, prot_flag=flag, y_a=ya, y_a_hat=yah,
+                                         s_bar=sb, s_hat=sh, out=out)
+    call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    es = yv.element_size()
+    nbytes = (2 * w.B * w.L_v * C + 2 * w.B * w.L_a * C) * es + w.B * w.L_v * (1 + 2 * 4)
+    del yv, yvh, ya, yah
+    torch.cuda.empty_cache()
+    return e0.elapsed_time(e1) / steps, nbytes
 
 
 def time_attention(plan, t, kv_idx, kv_cnt, steps, torch, sa):
@@ -361,6 +398,13 @@ def main():
             "dense_rows_kernel": "sparse_attn_bf16_kernel<128,128,gather>",
             "dense_rows_tflops": round(rows_tf, 2),
             "dense_rows_frac_of_peak": round(rows_tf / PEAK_BF16_TFLOPS, 4)}
+    if not args.no_cache_indicator:
+        ci_ms, ci_bytes = time_cache_indicator(w, args.steps, torch, sa)
+        ci_gbs = ci_bytes / (ci_ms * 1e-3) / 1e9
+        res["cache_indicator"] = {
+            "ms": round(ci_ms, 4), "channels": w.H * w.d, "bytes": ci_bytes,
+            "bound": "hbm", "achieved_gbs": round(ci_gbs, 1), "peak_gbs": PEAK_HBM_GBS,
+            "frac": round(ci_gbs / PEAK_HBM_GBS, 4)}
     if args.sweep:
         run_sweep(args.sweep, max(3, args.dense_steps), torch, sa, synth, LayerPlan)
     if not args.no_cpu_baseline:

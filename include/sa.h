@@ -21,7 +21,10 @@
  *   6. sa_select_protected_tokens   -- protected query tokens by top-k of the
  *                                      token saliency (Eq. (3)/(8));
  *   7. sa_protected_token_attention -- dense rows of the protected tokens
- *                                      over the sparse output (Eq. (9)-(11)).
+ *                                      over the sparse output (Eq. (9)-(11));
+ * and the cache-reuse decision:
+ *   8. sa_cache_indicator           -- synchronization-aware cache-reuse
+ *                                      indicator (Sec. 4.3, Eq. (12)-(15)).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -67,7 +70,8 @@ enum {
   SA_CALL_CROSS_SCORES = 0,
   SA_CALL_BUILD_BLOCK_MASK = 1,
   SA_CALL_SPARSE_ATTENTION = 2,
-  SA_CALL_SELECT_PROTECTED = 3
+  SA_CALL_SELECT_PROTECTED = 3,
+  SA_CALL_CACHE_INDICATOR = 4
 };
 
 /*
@@ -224,8 +228,41 @@ int sa_protected_token_attention(const void* q, const void* k, const void* v,
                                  void* stream);
 
 /*
+ * sa_cache_indicator -- synchronization-aware cache-reuse indicator of one
+ * block at one denoising step (Sec. 4.3, Eq. (12)-(15)).
+ *
+ *   dv = ||Y^v - Yh^v||_1 / (||Y^v||_1 + eps)                     Eq. (12)
+ *   da = the same for the audio outputs                             Eq. (12)
+ *   dp = dv restricted to the rows of protected video tokens        Eq. (13)
+ *   ds = 1 - <s_bar, s_hat> / (||s_bar||_2 ||s_hat||_2 + eps)       Eq. (14)
+ *   sync = max(dv, da, lambda_p * dp, lambda_s * ds)                Eq. (15)
+ *   reuse = sync < tau (decided on the fp32 value written to out[4])
+ * Every norm runs over the whole output (all batch items and channels):
+ * one decision per (step, block).  A NULL pair (audio, saliency, protected
+ * flags) contributes 0 to the max.  The paper uses lambda_p = 0.5,
+ * lambda_s = 0.1, tau = 0.2; eps is not given there.
+ *
+ *   y_v, y_v_hat   [B,L_v,C] in dtype: current and cached video block outputs
+ *   prot_flag      [B,L_v] u8, nonzero = protected token row, nullable
+ *   y_a, y_a_hat   [B,L_a,C] in dtype, both NULL or both non-NULL (L_a >= 1)
+ *   s_bar, s_hat   [B,L_v] f32 current and cached saliency, both NULL or both
+ *   C              channels per row, >= 8 and a multiple of 8
+ *   out            [6] f32 out (device): dv, da, dp, ds, sync, reuse (1 or 0)
+ *   ws             workspace of at least sa_workspace_size(SA_CALL_CACHE_INDICATOR)
+ */
+int sa_cache_indicator(const void* y_v, const void* y_v_hat,
+                       const uint8_t* prot_flag, const void* y_a,
+                       const void* y_a_hat, const float* s_bar,
+                       const float* s_hat, int B, int L_v, int L_a, int C,
+                       int dtype, float lambda_p, float lambda_s, float tau,
+                       float eps, float* out, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/*
  * Minimum workspace bytes of a call (SA_CALL_*) at the given sizes; L_a is
- * read by SA_CALL_CROSS_SCORES only.  Returns 0 for sizes the call rejects.
+ * read by SA_CALL_CROSS_SCORES and SA_CALL_CACHE_INDICATOR (0 = no audio),
+ * and SA_CALL_CACHE_INDICATOR reads B, L_v and L_a only.  Returns 0 for
+ * sizes the call rejects.
  * The figure covers both dtypes.
  */
 size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d,

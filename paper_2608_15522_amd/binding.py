@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsa.so")
 SA_OK, SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP = range(5)
 SA_BF16, SA_F32 = 0, 1
 (SA_CALL_CROSS_SCORES, SA_CALL_BUILD_BLOCK_MASK, SA_CALL_SPARSE_ATTENTION,
- SA_CALL_SELECT_PROTECTED) = range(4)
+ SA_CALL_SELECT_PROTECTED, SA_CALL_CACHE_INDICATOR) = range(5)
 
 # Every symbol the C header declares, with its ctypes signature.
 _VP, _I, _F, _SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
@@ -36,6 +36,8 @@ SIGNATURES = {
     "sa_select_protected_tokens": (_I, [_VP, _I, _I, _I, _VP, _VP, _VP]),
     "sa_protected_token_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
                                           _F, _VP, _I, _VP]),
+    "sa_cache_indicator": (_I, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
+                                _F, _F, _F, _F, _VP, _VP, _SZ, _VP]),
     "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "sa_last_error": (ctypes.c_char_p, []),
     "sa_version": (_I, []),
@@ -225,6 +227,27 @@ def sa_protected_token_attention(q, k, v, scale, tok_idx, o, lse=None):
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
         float(scale), _ptr(tok_idx) if k_tok > 0 else None, int(k_tok), _stream()))
     return o, lse
+
+
+def sa_cache_indicator(y_v, y_v_hat, *, prot_flag=None, y_a=None, y_a_hat=None,
+                       s_bar=None, s_hat=None, lambda_p=0.5, lambda_s=0.1, tau=0.2,
+                       eps=1e-6, out=None, ws=None):
+    """Cache-reuse indicator; returns out [6] f32 (device): dv, da, dp, ds,
+    sync, reuse."""
+    B, L_v, C = y_v.shape
+    L_a = y_a.shape[1] if y_a is not None else 0
+    dev = y_v.device
+    if out is None:
+        out = torch.empty(6, dtype=torch.float32, device=dev)
+    need = sa_workspace_size(SA_CALL_CACHE_INDICATOR, B, 1, L_v, L_a, 128, 128)
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check(lib().sa_cache_indicator(
+        _ptr(y_v), _ptr(y_v_hat), _ptr(prot_flag), _ptr(y_a), _ptr(y_a_hat),
+        _ptr(s_bar), _ptr(s_hat), B, L_v, L_a, C, _dtype_code(y_v), float(lambda_p),
+        float(lambda_s), float(tau), float(eps), _ptr(out), _ptr(ws), ws.numel(),
+        _stream()))
+    return out
 
 
 # ---- measurement helper library (libsa_bench.so, include/sa_bench.h) --------

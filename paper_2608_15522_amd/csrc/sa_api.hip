@@ -98,6 +98,8 @@ int sa_version(void) { return 100; }
 const char* sa_last_error(void) { return g_last_error.c_str(); }
 
 size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d, int block) {
+  if (call == SA_CALL_CACHE_INDICATOR)
+    return (B < 1 || L_v < 1 || L_a < 0) ? 0 : sa::cache_ws_bytes(B, L_v, L_a);
   if (B < 1 || H < 1 || L_v < 1 || (d != 64 && d != 128) || (block != 64 && block != 128))
     return 0;
   const int n_b = sa::ceil_div(L_v, block);
@@ -281,6 +283,49 @@ int sa_protected_token_attention(const void* q, const void* k, const void* v, vo
         static_cast<const float*>(q), static_cast<const float*>(k),
         static_cast<const float*>(v), static_cast<float*>(o), lse, B, H, L, d, scale,
         tok_idx, k_tok, s);
+  return check_launch(fn);
+}
+
+int sa_cache_indicator(const void* y_v, const void* y_v_hat, const uint8_t* prot_flag,
+                       const void* y_a, const void* y_a_hat, const float* s_bar,
+                       const float* s_hat, int B, int L_v, int L_a, int C, int dtype,
+                       float lambda_p, float lambda_s, float tau, float eps, float* out,
+                       void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sa_cache_indicator";
+  if (B < 1 || L_v < 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: B=%d L_v=%d must be >= 1", fn, B, L_v);
+  if (dtype != SA_BF16 && dtype != SA_F32)
+    return fail(SA_ERR_UNSUPPORTED, "%s: dtype %d is neither SA_BF16 nor SA_F32", fn, dtype);
+  if (C < 8 || C % 8 != 0)
+    return fail(SA_ERR_INVALID_ARG, "%s: C=%d must be >= 8 and a multiple of 8", fn, C);
+  if ((y_a == nullptr) != (y_a_hat == nullptr))
+    return fail(SA_ERR_INVALID_ARG, "%s: y_a and y_a_hat must be both NULL or both non-NULL",
+                fn);
+  if (y_a != nullptr && L_a < 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: L_a=%d must be >= 1 with audio outputs", fn, L_a);
+  if ((s_bar == nullptr) != (s_hat == nullptr))
+    return fail(SA_ERR_INVALID_ARG, "%s: s_bar and s_hat must be both NULL or both non-NULL",
+                fn);
+  if (!(lambda_p >= 0.f) || !isfinite(lambda_p) || !(lambda_s >= 0.f) || !isfinite(lambda_s) ||
+      !isfinite(tau) || !(eps >= 0.f) || !isfinite(eps))
+    return fail(SA_ERR_INVALID_ARG,
+                "%s: lambda_p=%g lambda_s=%g must be finite and >= 0, tau=%g finite, "
+                "eps=%g finite and >= 0", fn, static_cast<double>(lambda_p),
+                static_cast<double>(lambda_s), static_cast<double>(tau),
+                static_cast<double>(eps));
+  SA_TRY(check_tensor(fn, "y_v", y_v, true, 16));
+  SA_TRY(check_tensor(fn, "y_v_hat", y_v_hat, true, 16));
+  SA_TRY(check_tensor(fn, "prot_flag", prot_flag, false, 1));
+  SA_TRY(check_tensor(fn, "y_a", y_a, false, 16));
+  SA_TRY(check_tensor(fn, "y_a_hat", y_a_hat, false, 16));
+  SA_TRY(check_tensor(fn, "s_bar", s_bar, false, 4));
+  SA_TRY(check_tensor(fn, "s_hat", s_hat, false, 4));
+  SA_TRY(check_tensor(fn, "out", out, true, 4));
+  const int la = y_a != nullptr ? L_a : 0;
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::cache_ws_bytes(B, L_v, la)));
+  sa::launch_cache_indicator(y_v, y_v_hat, prot_flag, y_a, y_a_hat, s_bar, s_hat, B, L_v, la,
+                             C, dtype, lambda_p, lambda_s, tau, eps, out,
+                             static_cast<char*>(ws), static_cast<hipStream_t>(stream));
   return check_launch(fn);
 }
 

@@ -82,6 +82,20 @@ inline AttnWs attn_ws_layout(int B, int H, int n_b, int /*d*/, int /*block*/) {
 
 // ---- launchers (defined in the kernel sources) ----------------------------
 constexpr int kMaxTokens = kMaxBlocks * 128;  // longest token sequence (L)
+// Cache-reuse indicator: 9 fp32 partial sums per workgroup of the first pass
+// ([9][workgroups]).
+int cache_workgroups_video(size_t rows_v);
+int cache_workgroups_audio(size_t rows_a);
+inline size_t cache_ws_bytes(int B, int L_v, int L_a) {
+  const size_t nwg = static_cast<size_t>(cache_workgroups_video(static_cast<size_t>(B) * L_v)) +
+                     cache_workgroups_audio(static_cast<size_t>(B) * (L_a > 0 ? L_a : 0)) + 1;
+  return align_up(nwg * 9 * sizeof(float));
+}
+void launch_cache_indicator(const void* y_v, const void* y_v_hat, const uint8_t* prot_flag,
+                            const void* y_a, const void* y_a_hat, const float* s_bar,
+                            const float* s_hat, int B, int L_v, int L_a, int C, int dtype,
+                            float lambda_p, float lambda_s, float tau, float eps,
+                            float* out, char* ws, hipStream_t s);
 void launch_saliency_ema(float* s_bar, const float* s, size_t n, float alpha,
                          hipStream_t st);
 void launch_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,

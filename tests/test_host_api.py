@@ -64,6 +64,11 @@ def test_workspace_sizes():
         assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, *bad) == 0
     assert sa.sa_workspace_size(sa.SA_CALL_CROSS_SCORES, 1, 1, 10, 0, 64, 64) == 0
     assert sa.sa_workspace_size(9, 1, 1, 10, 1, 64, 64) == 0
+    # cache indicator: 9 fp32 partials per workgroup (1024 video, 64 audio, 1)
+    assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 1, 0, 32760, 512, 0, 0) == \
+        ((1024 + 64 + 1) * 36 + 255) // 256 * 256
+    assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 1, 0, 10, 0, 0, 0) == 512
+    assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 0, 0, 10, 0, 0, 0) == 0
 
 
 def _attn(**kw):
@@ -118,7 +123,29 @@ def _ptok(**kw):
     return sa.lib().sa_protected_token_attention(*a.values())
 
 
+def _cache(**kw):
+    a = dict(y_v=FAKE, y_v_hat=FAKE, prot_flag=None, y_a=None, y_a_hat=None,
+             s_bar=None, s_hat=None, B=1, L_v=1000, L_a=0, C=64, dtype=0,
+             lambda_p=0.5, lambda_s=0.1, tau=0.2, eps=1e-6, out=FAKE, ws=FAKE,
+             ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return sa.lib().sa_cache_indicator(*a.values())
+
+
 @pytest.mark.parametrize("call,kw,code,needle", [
+    (_cache, dict(C=12), sa.SA_ERR_INVALID_ARG, "multiple of 8"),
+    (_cache, dict(C=0), sa.SA_ERR_INVALID_ARG, "multiple of 8"),
+    (_cache, dict(L_v=0), sa.SA_ERR_INVALID_ARG, "L_v=0"),
+    (_cache, dict(dtype=3), sa.SA_ERR_UNSUPPORTED, "dtype"),
+    (_cache, dict(y_a=FAKE), sa.SA_ERR_INVALID_ARG, "y_a and y_a_hat"),
+    (_cache, dict(y_a=FAKE, y_a_hat=FAKE, L_a=0), sa.SA_ERR_INVALID_ARG, "L_a=0"),
+    (_cache, dict(s_hat=FAKE), sa.SA_ERR_INVALID_ARG, "s_bar and s_hat"),
+    (_cache, dict(eps=-1.0), sa.SA_ERR_INVALID_ARG, "eps"),
+    (_cache, dict(tau=float("nan")), sa.SA_ERR_INVALID_ARG, "tau"),
+    (_cache, dict(lambda_p=float("inf")), sa.SA_ERR_INVALID_ARG, "lambda_p"),
+    (_cache, dict(out=None), sa.SA_ERR_INVALID_ARG, "out is NULL"),
+    (_cache, dict(y_v_hat=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_cache, dict(ws_bytes=4), sa.SA_ERR_WORKSPACE, "workspace"),
     (_ema, dict(alpha=1.5), sa.SA_ERR_INVALID_ARG, "alpha"),
     (_ema, dict(alpha=float("nan")), sa.SA_ERR_INVALID_ARG, "alpha"),
     (_ema, dict(sal_bar=None), sa.SA_ERR_INVALID_ARG, "sal_bar is NULL"),
