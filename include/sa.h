@@ -246,7 +246,10 @@ int sa_protected_token_attention(const void* q, const void* k, const void* v,
  *   prot_flag      [B,L_v] u8, nonzero = protected token row, nullable
  *   y_a, y_a_hat   [B,L_a,C] in dtype, both NULL or both non-NULL (L_a >= 1)
  *   s_bar, s_hat   [B,L_v] f32 current and cached saliency, both NULL or both
- *   C              channels per row, >= 8 and a multiple of 8
+ *   C              channels per row, >= 8 and a multiple of 8; a
+ *                  workgroup's share (ceil(B*L_v/1024) video rows, ceil(B*L_a/64)
+ *                  audio rows) holds at most 2^32 - 1 chunks of 16 bytes, else
+ *                  SA_ERR_INVALID_ARG
  *   out            [6] f32 out (device): dv, da, dp, ds, sync, reuse (1 or 0)
  *   ws             workspace of at least sa_workspace_size(SA_CALL_CACHE_INDICATOR)
  */

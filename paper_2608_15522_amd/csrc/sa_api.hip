@@ -322,6 +322,14 @@ int sa_cache_indicator(const void* y_v, const void* y_v_hat, const uint8_t* prot
   SA_TRY(check_tensor(fn, "s_hat", s_hat, false, 4));
   SA_TRY(check_tensor(fn, "out", out, true, 4));
   const int la = y_a != nullptr ? L_a : 0;
+  // a workgroup indexes its span of 16-byte chunks with 32 bits
+  const size_t cpr = static_cast<size_t>(C) / (dtype == SA_BF16 ? 8 : 4);
+  const size_t rv = static_cast<size_t>(B) * L_v, ra = static_cast<size_t>(B) * la;
+  const size_t wv = sa::cache_workgroups_video(rv), wa = sa::cache_workgroups_audio(ra);
+  if ((rv + wv - 1) / wv * cpr > 0xffffffffull ||
+      (wa > 0 && (ra + wa - 1) / wa * cpr > 0xffffffffull))
+    return fail(SA_ERR_INVALID_ARG, "%s: B=%d L_v=%d L_a=%d C=%d is too large", fn, B, L_v,
+                la, C);
   SA_TRY(check_ws(fn, ws, ws_bytes, sa::cache_ws_bytes(B, L_v, la)));
   sa::launch_cache_indicator(y_v, y_v_hat, prot_flag, y_a, y_a_hat, s_bar, s_hat, B, L_v, la,
                              C, dtype, lambda_p, lambda_s, tau, eps, out,

@@ -1,9 +1,9 @@
 // Synchronization-aware cache-reuse indicator (Sec. 4.3, Eq. (12)-(15)).
 //
 // K10 cache_partial: one pass over the block outputs.  Workgroups
-//     [0, wg_v) share the video rows (B*L_v rows of C channels),
-//     [wg_v, wg_v + wg_a) the audio rows, and the last one the two saliency
-//     maps.  Each thread adds |Y - Y_hat| and |Y| (and the same on rows of
+//     [0, wg_v) share the video rows (B*L_v rows of C channels) and the
+//     matching entries of the two saliency maps, [wg_v, wg_v + wg_a) the
+//     audio rows.  Each thread adds |Y - Y_hat| and |Y| (and the same on rows of
 //     protected tokens) in fp32 over its 16-byte chunks; the workgroup sums
 //     are formed in a fixed order and written as 9 partials per
 //     workgroup ([9][workgroups]): video diff/mag, protected diff/mag, audio
@@ -64,67 +64,59 @@ __device__ __forceinline__ void block_sums(A (&acc)[kCacheParts], A (*red)[kCach
 
 // |y - y_hat| and |y| over rows [r0, r1) of [rows][C] (C a multiple of the
 // chunk width); rows with flag[row] != 0 also count into the second pair.
-// The 16-byte chunks of a row are spread over the workgroup; a step takes
-// RU rows x U chunks per thread, so up to 2*RU*U loads are in flight.
+// The rows are one contiguous span of 16-byte chunks, dealt out to the
+// threads in steps of U chunks each (2*U loads in flight per thread); the
+// host keeps (r1 - r0) * C / chunk below 2^32.
 template <typename T>
 __device__ __forceinline__ void rows_l1(const T* y, const T* yh, const uint8_t* flag,
                                         size_t r0, size_t r1, int C, float* acc) {
   constexpr int EPC = Chunk<T>::kElems;
-  constexpr int RU = 4, U = 2;
-  const int cpr = C / EPC;
-  for (size_t row0 = r0; row0 < r1; row0 += RU) {
-    bool prot[RU];
+  constexpr int U = 8;
+  const uint32_t cpr = static_cast<uint32_t>(C / EPC);
+  const uint32_t n = static_cast<uint32_t>((r1 - r0) * cpr);
+  const T* ya = y + r0 * C;
+  const T* yb = yh + r0 * C;
+  for (uint32_t j0 = threadIdx.x; j0 < n; j0 += U * kCacheThreads) {
+    u32x4 va[U], vb[U];
+    bool pr[U];
 #pragma unroll
-    for (int k = 0; k < RU; ++k)
-      prot[k] = flag != nullptr && row0 + k < r1 && flag[row0 + k] != 0;
-    float dsum[RU], msum[RU];
-#pragma unroll
-    for (int k = 0; k < RU; ++k) dsum[k] = msum[k] = 0.f;
-    for (int c0 = threadIdx.x; c0 < cpr; c0 += U * kCacheThreads) {
-      u32x4 va[RU][U], vb[RU][U];
-#pragma unroll
-      for (int k = 0; k < RU; ++k)
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int c = c0 + u * kCacheThreads;
-          const bool ok = row0 + k < r1 && c < cpr;
-          const size_t off = (row0 + k) * C + static_cast<size_t>(c) * EPC;
-          va[k][u] = ok ? ldg16(y + off) : u32x4{0u, 0u, 0u, 0u};
-          vb[k][u] = ok ? ldg16(yh + off) : u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-      for (int k = 0; k < RU; ++k)
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          float a[EPC], b[EPC];
-          Chunk<T>::unpack(va[k][u], a);
-          Chunk<T>::unpack(vb[k][u], b);
-#pragma unroll
-          for (int e = 0; e < EPC; ++e) {
-            dsum[k] += fabsf(a[e] - b[e]);
-            msum[k] += fabsf(a[e]);
-          }
-        }
+    for (int u = 0; u < U; ++u) {
+      const uint32_t j = j0 + u * kCacheThreads;
+      const bool ok = j < n;
+      va[u] = ok ? ldg16(ya + static_cast<size_t>(j) * EPC) : u32x4{0u, 0u, 0u, 0u};
+      vb[u] = ok ? ldg16(yb + static_cast<size_t>(j) * EPC) : u32x4{0u, 0u, 0u, 0u};
+      pr[u] = flag != nullptr && ok && flag[r0 + j / cpr] != 0;
     }
 #pragma unroll
-    for (int k = 0; k < RU; ++k) {
-      acc[0] += dsum[k];
-      acc[1] += msum[k];
-      if (prot[k]) {
-        acc[2] += dsum[k];
-        acc[3] += msum[k];
+    for (int u = 0; u < U; ++u) {
+      float a[EPC], b[EPC];
+      Chunk<T>::unpack(va[u], a);
+      Chunk<T>::unpack(vb[u], b);
+      float d = 0.f, m = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        d += fabsf(a[e] - b[e]);
+        m += fabsf(a[e]);
+      }
+      acc[0] += d;
+      acc[1] += m;
+      if (pr[u]) {
+        acc[2] += d;
+        acc[3] += m;
       }
     }
   }
 }
 
+// Video workgroup wg owns rows [r0, r1) of the B*L_v video rows and the same
+// entries of the two [B, L_v] saliency maps; audio workgroups own audio rows.
 template <typename T>
 __global__ void __launch_bounds__(kCacheThreads)
 cache_partial_kernel(const T* __restrict__ yv, const T* __restrict__ yvh,
                      const uint8_t* __restrict__ pflag, size_t rows_v, int C,
                      const T* __restrict__ ya, const T* __restrict__ yah, size_t rows_a,
-                     const float* __restrict__ sb, const float* __restrict__ sh,
-                     size_t n_s, int wg_v, int wg_a, float* __restrict__ part) {
+                     const float* __restrict__ sb, const float* __restrict__ sh, int wg_v,
+                     int wg_a, float* __restrict__ part) {
   __shared__ float red[kCacheThreads / 64][kCacheParts];
   const int wg = blockIdx.x;
   float acc[kCacheParts];
@@ -132,21 +124,22 @@ cache_partial_kernel(const T* __restrict__ yv, const T* __restrict__ yvh,
   for (int j = 0; j < kCacheParts; ++j) acc[j] = 0.f;
   if (wg < wg_v) {
     const size_t r0 = rows_v * wg / wg_v, r1 = rows_v * (wg + 1) / wg_v;
+    if (sb != nullptr) {
+      for (size_t i = r0 + threadIdx.x; i < r1; i += kCacheThreads) {
+        const float x = sb[i], z = sh[i];
+        acc[6] = fmaf(x, z, acc[6]);
+        acc[7] = fmaf(x, x, acc[7]);
+        acc[8] = fmaf(z, z, acc[8]);
+      }
+    }
     rows_l1(yv, yvh, pflag, r0, r1, C, acc);
-  } else if (wg < wg_v + wg_a) {
+  } else {
     const int a = wg - wg_v;
     const size_t r0 = rows_a * a / wg_a, r1 = rows_a * (a + 1) / wg_a;
     float tmp[4] = {0.f, 0.f, 0.f, 0.f};
     rows_l1<T>(ya, yah, nullptr, r0, r1, C, tmp);
     acc[4] = tmp[0];
     acc[5] = tmp[1];
-  } else if (sb != nullptr) {
-    for (size_t i = threadIdx.x; i < n_s; i += kCacheThreads) {
-      const float x = sb[i], z = sh[i];
-      acc[6] = fmaf(x, z, acc[6]);
-      acc[7] = fmaf(x, x, acc[7]);
-      acc[8] = fmaf(z, z, acc[8]);
-    }
   }
   block_sums(acc, red);
   if (threadIdx.x == 0) {
@@ -213,20 +206,19 @@ void launch_cache_indicator(const void* y_v, const void* y_v_hat, const uint8_t*
   const size_t rows_a = y_a != nullptr ? static_cast<size_t>(B) * L_a : 0;
   const int wg_v = cache_workgroups_video(rows_v);
   const int wg_a = cache_workgroups_audio(rows_a);
-  const int nwg = wg_v + wg_a + 1;
+  const int nwg = wg_v + wg_a;
   float* part = reinterpret_cast<float*>(ws);
-  const size_t n_s = static_cast<size_t>(B) * L_v;
   if (dtype == 0)
     hipLaunchKernelGGL(cache_partial_kernel<uint16_t>, dim3(nwg), dim3(kCacheThreads), 0, s,
                        static_cast<const uint16_t*>(y_v), static_cast<const uint16_t*>(y_v_hat),
                        prot_flag, rows_v, C, static_cast<const uint16_t*>(y_a),
-                       static_cast<const uint16_t*>(y_a_hat), rows_a, s_bar, s_hat, n_s, wg_v,
+                       static_cast<const uint16_t*>(y_a_hat), rows_a, s_bar, s_hat, wg_v,
                        wg_a, part);
   else
     hipLaunchKernelGGL(cache_partial_kernel<float>, dim3(nwg), dim3(kCacheThreads), 0, s,
                        static_cast<const float*>(y_v), static_cast<const float*>(y_v_hat),
                        prot_flag, rows_v, C, static_cast<const float*>(y_a),
-                       static_cast<const float*>(y_a_hat), rows_a, s_bar, s_hat, n_s, wg_v,
+                       static_cast<const float*>(y_a_hat), rows_a, s_bar, s_hat, wg_v,
                        wg_a, part);
   hipLaunchKernelGGL(cache_finish_kernel, dim3(1), dim3(kFinishThreads), 0, s, part, nwg,
                      prot_flag != nullptr, y_a != nullptr, s_bar != nullptr, lambda_p,

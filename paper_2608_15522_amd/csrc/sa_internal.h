@@ -88,7 +88,7 @@ int cache_workgroups_video(size_t rows_v);
 int cache_workgroups_audio(size_t rows_a);
 inline size_t cache_ws_bytes(int B, int L_v, int L_a) {
   const size_t nwg = static_cast<size_t>(cache_workgroups_video(static_cast<size_t>(B) * L_v)) +
-                     cache_workgroups_audio(static_cast<size_t>(B) * (L_a > 0 ? L_a : 0)) + 1;
+                     cache_workgroups_audio(static_cast<size_t>(B) * (L_a > 0 ? L_a : 0));
   return align_up(nwg * 9 * sizeof(float));
 }
 void launch_cache_indicator(const void* y_v, const void* y_v_hat, const uint8_t* prot_flag,

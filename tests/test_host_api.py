@@ -64,9 +64,9 @@ def test_workspace_sizes():
         assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, *bad) == 0
     assert sa.sa_workspace_size(sa.SA_CALL_CROSS_SCORES, 1, 1, 10, 0, 64, 64) == 0
     assert sa.sa_workspace_size(9, 1, 1, 10, 1, 64, 64) == 0
-    # cache indicator: 9 fp32 partials per workgroup (1024 video, 64 audio, 1)
+    # cache indicator: 9 fp32 partials per workgroup (1024 video, 64 audio)
     assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 1, 0, 32760, 512, 0, 0) == \
-        ((1024 + 64 + 1) * 36 + 255) // 256 * 256
+        ((1024 + 64) * 36 + 255) // 256 * 256
     assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 1, 0, 10, 0, 0, 0) == 512
     assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 0, 0, 10, 0, 0, 0) == 0
 
@@ -135,6 +135,7 @@ def _cache(**kw):
 @pytest.mark.parametrize("call,kw,code,needle", [
     (_cache, dict(C=12), sa.SA_ERR_INVALID_ARG, "multiple of 8"),
     (_cache, dict(C=0), sa.SA_ERR_INVALID_ARG, "multiple of 8"),
+    (_cache, dict(B=1 << 20, L_v=1 << 10, C=1 << 16), sa.SA_ERR_INVALID_ARG, "too large"),
     (_cache, dict(L_v=0), sa.SA_ERR_INVALID_ARG, "L_v=0"),
     (_cache, dict(dtype=3), sa.SA_ERR_UNSUPPORTED, "dtype"),
     (_cache, dict(y_a=FAKE), sa.SA_ERR_INVALID_ARG, "y_a and y_a_hat"),
