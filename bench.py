@@ -144,6 +144,9 @@ def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
     kv_idx = torch.empty_like(plan.kv_idx)
     kv_cnt = torch.empty_like(plan.kv_cnt)
     o = torch.empty_like(t["q_v"])
+    tok_ws = torch.empty(max(1, sa.sa_workspace_size(sa.SA_CALL_TOKEN_ATTENTION, w.B, w.H, w.L_v,
+                                                     k_tok, w.d, 0)),
+                         dtype=torch.uint8, device=dev)
     names = ["sa_cross_scores", "sa_saliency_ema", "sa_select_protected_tokens",
              "sa_build_block_mask", "sa_sparse_attention", "sa_protected_token_attention"]
 
@@ -163,7 +166,7 @@ def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
                                kv_idx, kv_cnt, o=o, ws=plan.ws)
         rec(5)
         sa.sa_protected_token_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale,
-                                        tok_idx, o)
+                                        tok_idx, o, ws=tok_ws)
         rec(6)
 
     for _ in range(warmup):

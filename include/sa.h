@@ -71,7 +71,8 @@ enum {
   SA_CALL_BUILD_BLOCK_MASK = 1,
   SA_CALL_SPARSE_ATTENTION = 2,
   SA_CALL_SELECT_PROTECTED = 3,
-  SA_CALL_CACHE_INDICATOR = 4
+  SA_CALL_CACHE_INDICATOR = 4,
+  SA_CALL_TOKEN_ATTENTION = 5
 };
 
 /*
@@ -219,13 +220,17 @@ int sa_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,
  *   lse        [B,H,L] f32 in/out, nullable
  *   tok_idx    [B,k_tok] i32; entries outside [0,L) are skipped
  *   k_tok      0 <= k_tok <= L; 0 = nothing to do
- * No workspace.
+ *   ws         workspace of at least sa_workspace_size(SA_CALL_TOKEN_ATTENTION,
+ *              B, H, L, k_tok, d, 0) bytes (0 when the keys of a row are not
+ *              split: then ws may be NULL).  With bf16 inputs the keys of each
+ *              row may be cut into up to 8 runs whose partial rows (f32) are
+ *              merged in a fixed order, so results do not depend on timing.
  */
 int sa_protected_token_attention(const void* q, const void* k, const void* v,
                                  void* o, float* lse, int B, int H, int L,
                                  int d, int dtype, float scale,
-                                 const int32_t* tok_idx, int k_tok,
-                                 void* stream);
+                                 const int32_t* tok_idx, int k_tok, void* ws,
+                                 size_t ws_bytes, void* stream);
 
 /*
  * sa_cache_indicator -- synchronization-aware cache-reuse indicator of one
@@ -264,8 +269,10 @@ int sa_cache_indicator(const void* y_v, const void* y_v_hat,
 /*
  * Minimum workspace bytes of a call (SA_CALL_*) at the given sizes; L_a is
  * read by SA_CALL_CROSS_SCORES and SA_CALL_CACHE_INDICATOR (0 = no audio),
- * and SA_CALL_CACHE_INDICATOR reads B, L_v and L_a only.  Returns 0 for
- * sizes the call rejects.
+ * and SA_CALL_CACHE_INDICATOR reads B, L_v and L_a only.
+ * SA_CALL_TOKEN_ATTENTION reads B, H, L_v (the sequence length L), d and
+ * k_tok in the place of L_a; block is not read.  Returns 0 for sizes the
+ * call rejects.
  * The figure covers both dtypes.
  */
 size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d,

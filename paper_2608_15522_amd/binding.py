@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsa.so")
 SA_OK, SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP = range(5)
 SA_BF16, SA_F32 = 0, 1
 (SA_CALL_CROSS_SCORES, SA_CALL_BUILD_BLOCK_MASK, SA_CALL_SPARSE_ATTENTION,
- SA_CALL_SELECT_PROTECTED, SA_CALL_CACHE_INDICATOR) = range(5)
+ SA_CALL_SELECT_PROTECTED, SA_CALL_CACHE_INDICATOR, SA_CALL_TOKEN_ATTENTION) = range(6)
 
 # Every symbol the C header declares, with its ctypes signature.
 _VP, _I, _F, _SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
@@ -35,7 +35,7 @@ SIGNATURES = {
     "sa_saliency_ema": (_I, [_VP, _VP, _SZ, _F, _VP]),
     "sa_select_protected_tokens": (_I, [_VP, _I, _I, _I, _VP, _VP, _VP]),
     "sa_protected_token_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
-                                          _F, _VP, _I, _VP]),
+                                          _F, _VP, _I, _VP, _SZ, _VP]),
     "sa_cache_indicator": (_I, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
                                 _F, _F, _F, _F, _VP, _VP, _SZ, _VP]),
     "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
@@ -219,13 +219,15 @@ def sa_select_protected_tokens(sal_tok, k_tok, *, tok_idx=None, tok_flag=None,
     return tok_idx, tok_flag
 
 
-def sa_protected_token_attention(q, k, v, scale, tok_idx, o, lse=None):
+def sa_protected_token_attention(q, k, v, scale, tok_idx, o, lse=None, *, ws=None):
     """Dense rows of the protected tokens written over o (and lse); returns (o, lse)."""
     B, H, L, d = q.shape
     k_tok = tok_idx.shape[1]
+    ws = _workspace(SA_CALL_TOKEN_ATTENTION, B, H, L, k_tok, d, 0, q.device, ws)
     _check(lib().sa_protected_token_attention(
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
-        float(scale), _ptr(tok_idx) if k_tok > 0 else None, int(k_tok), _stream()))
+        float(scale), _ptr(tok_idx) if k_tok > 0 else None, int(k_tok), _ptr(ws),
+        ws.numel(), _stream()))
     return o, lse
 
 

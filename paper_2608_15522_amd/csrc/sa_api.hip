@@ -100,6 +100,12 @@ const char* sa_last_error(void) { return g_last_error.c_str(); }
 size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d, int block) {
   if (call == SA_CALL_CACHE_INDICATOR)
     return (B < 1 || L_v < 1 || L_a < 0) ? 0 : sa::cache_ws_bytes(B, L_v, L_a);
+  if (call == SA_CALL_TOKEN_ATTENTION) {  // L_a carries k_tok
+    if (B < 1 || H < 1 || L_v < 1 || L_v > sa::kMaxTokens || (d != 64 && d != 128) ||
+        L_a < 0 || L_a > L_v)
+      return 0;
+    return sa::token_attn_ws_bytes(B, H, L_v, d, L_a);
+  }
   if (B < 1 || H < 1 || L_v < 1 || (d != 64 && d != 128) || (block != 64 && block != 128))
     return 0;
   const int n_b = sa::ceil_div(L_v, block);
@@ -259,8 +265,8 @@ int sa_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,
 
 int sa_protected_token_attention(const void* q, const void* k, const void* v, void* o,
                                  float* lse, int B, int H, int L, int d, int dtype,
-                                 float scale, const int32_t* tok_idx, int k_tok,
-                                 void* stream) {
+                                 float scale, const int32_t* tok_idx, int k_tok, void* ws,
+                                 size_t ws_bytes, void* stream) {
   const char* fn = "sa_protected_token_attention";
   SA_TRY(check_common(fn, B, H, L, d, dtype, scale, 128));
   if (k_tok < 0 || k_tok > L)
@@ -271,13 +277,14 @@ int sa_protected_token_attention(const void* q, const void* k, const void* v, vo
   SA_TRY(check_tensor(fn, "o", o, true, 16));
   SA_TRY(check_tensor(fn, "lse", lse, false, 4));
   SA_TRY(check_tensor(fn, "tok_idx", tok_idx, k_tok > 0, 4));
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::token_attn_ws_bytes(B, H, L, d, k_tok)));
   if (k_tok == 0) return ok();
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == SA_BF16)
     sa::launch_protected_token_attention_bf16(
         static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
         static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, B, H, L, d, scale,
-        tok_idx, k_tok, s);
+        tok_idx, k_tok, static_cast<char*>(ws), s);
   else
     sa::launch_protected_token_attention_f32(
         static_cast<const float*>(q), static_cast<const float*>(k),

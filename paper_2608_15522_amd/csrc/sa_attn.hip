@@ -83,8 +83,11 @@ __device__ __forceinline__ float max_halves(float x) {
 
 // GATHER (dense rows of protected tokens, Eq. (11) first case): workgroup row
 // j of pair (b,h) is token rows[b*n_rows + j] (rows >= n_rows, or a token
-// outside [0, L), are skipped); every key tile is kept; O and lse are written
-// to the token's own row.  kv_idx, kv_cnt and order are not read.
+// outside [0, L), are skipped); kv_idx, kv_cnt and order are not read.  The
+// key blocks are cut into n_split equal runs, one per workgroup: with
+// n_split == 1 the workgroup keeps every key and writes O and lse to the
+// token's own row; otherwise it writes its unnormalised O, running max m
+// (log2 units) and row sum to `part` for token_combine_kernel.
 template <int D, int BLOCK, bool GATHER>
 __global__ void __launch_bounds__(BLOCK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
@@ -95,7 +98,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         const int32_t* __restrict__ kv_cnt,
                         const int32_t* __restrict__ order, int P, int L,
                         int n_b, float c, const int32_t* __restrict__ rows, int n_rows,
-                        int H) {
+                        int H, int n_split, float* __restrict__ part) {
   constexpr int NW = BLOCK / 32;             // waves per workgroup
   constexpr int TPB = BLOCK / kTile;         // tiles per key block
   constexpr int KC = D / 16;                 // k-steps of Q K^T
@@ -119,7 +122,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   // XCD x works through its pairs x, x+8, ... one at a time, heaviest query
   // block first: the K/V blocks of the pair in flight are shared through that
   // XCD's L2, and only 8 pairs are live at once across the chip.
-  const int n_q = GATHER ? ceil_div(n_rows, BLOCK) : n_b;  // query blocks per pair
+  const int n_qr = GATHER ? ceil_div(n_rows, BLOCK) : n_b;  // query blocks per pair
+  const int n_q = GATHER ? n_qr * n_split : n_b;              // workgroups per pair
   int pair, rank;
   if ((P & 7) == 0) {
     const int i = blockIdx.x >> 3;
@@ -130,11 +134,14 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     rank = blockIdx.x / P;
   }
   const size_t row_base = static_cast<size_t>(pair) * n_b;
-  int r, cnt;
+  int r, cnt, kb0 = 0, split = 0;
   const int32_t* idx = nullptr;
   if constexpr (GATHER) {
-    r = rank;
-    cnt = n_b;
+    // consecutive ranks share a key run and so its K/V tiles in L2
+    split = rank / n_qr;
+    r = rank - split * n_qr;
+    kb0 = n_b * split / n_split;
+    cnt = n_b * (split + 1) / n_split - kb0;
   } else {
     r = order[row_base + rank];
     cnt = kv_cnt[row_base + r];
@@ -152,7 +159,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     const uint64_t below = (1ull << lane) - 1ull;
     for (int i0 = 0; i0 < cnt; i0 += 64) {
       const int i = i0 + lane;
-      const int kb = i < cnt ? (GATHER ? i : idx[i]) : -1;
+      const int kb = i < cnt ? (GATHER ? kb0 + i : idx[i]) : -1;
       const bool v0 = kb >= 0 && kb < n_b;
       const bool v1 = TPB == 2 && v0 && kb * BLOCK + kTile < L;
       const bool f0 = v0 && kb * BLOCK + kTile <= L;
@@ -515,6 +522,29 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   for (; t < T; ++t) iteration(t, CopyFlag<true>{});
 
   const float ltot = lsum + swap_halves(lsum);
+  if constexpr (GATHER) {
+    if (part != nullptr) {
+      if (qvalid) {
+        const size_t prow = static_cast<size_t>(split * P + pair) * n_rows +
+                            (r * BLOCK + (tid >> 6) * 32 + n);
+        float* orow = part + prow * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const f32x4 val = {acc[dt][4 * rg], acc[dt][4 * rg + 1], acc[dt][4 * rg + 2],
+                               acc[dt][4 * rg + 3]};
+            *reinterpret_cast<f32x4*>(orow + 32 * dt + 8 * rg + 4 * g) = val;
+          }
+        if (g == 0) {
+          float2* ml = reinterpret_cast<float2*>(
+              part + static_cast<size_t>(n_split) * P * n_rows * D);
+          ml[prow] = make_float2(m, ltot);
+        }
+      }
+      return;
+    }
+  }
   const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
   if (qvalid) {
     uint16_t* orow = o + (static_cast<size_t>(pair) * L + qrow) * D;
@@ -532,6 +562,48 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       lse[static_cast<size_t>(pair) * L + qrow] =
           ltot > 0.f ? (m + __log2f(ltot)) * kLn2 : -INFINITY;
   }
+}
+
+// Merges the n_split partial rows of each protected token: with M the
+// largest running max, O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s and
+// lse = (M + log2 of the denominator) ln 2, the splits added in index order.
+// One thread per 4 channels of a row.
+template <int D>
+__global__ void __launch_bounds__(256)
+token_combine_kernel(const float* __restrict__ part, int n_split, int P, int L, int H,
+                     const int32_t* __restrict__ rows, int n_rows, uint16_t* __restrict__ o,
+                     float* __restrict__ lse) {
+  constexpr int TPR = D / 4;
+  const size_t gid = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  const size_t pr = gid / TPR;  // pair * n_rows + j
+  if (pr >= static_cast<size_t>(P) * n_rows) return;
+  const int d4 = static_cast<int>(gid % TPR) * 4;
+  const int pair = static_cast<int>(pr / n_rows), j = static_cast<int>(pr % n_rows);
+  const int t = rows[static_cast<size_t>(pair / H) * n_rows + j];
+  if (t < 0 || t >= L) return;
+  const size_t stride = static_cast<size_t>(P) * n_rows;  // rows per split
+  const float2* ml = reinterpret_cast<const float2*>(part + n_split * stride * D);
+  float M = -INFINITY;
+  for (int s = 0; s < n_split; ++s) {
+    const float2 v = ml[s * stride + pr];
+    if (v.y > 0.f) M = fmaxf(M, v.x);
+  }
+  float den = 0.f;
+  f32x4 num = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < n_split; ++s) {
+    const float2 v = ml[s * stride + pr];
+    const float w = v.y > 0.f ? exp2f(v.x - M) : 0.f;
+    const f32x4 x = *reinterpret_cast<const f32x4*>(part + (s * stride + pr) * D + d4);
+    den = fmaf(w, v.y, den);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) num[e] = fmaf(w, x[e], num[e]);
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  const u32x2 val = {pack_bf16x2(num[0] * inv, num[1] * inv),
+                     pack_bf16x2(num[2] * inv, num[3] * inv)};
+  *reinterpret_cast<u32x2*>(o + (static_cast<size_t>(pair) * L + t) * D + d4) = val;
+  if (lse != nullptr && d4 == 0)
+    lse[static_cast<size_t>(pair) * L + t] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
 }
 
 // ---- fp32 path ------------------------------------------------------------
@@ -637,16 +709,20 @@ void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
   const dim3 grid(P * n_b);
   if (d == 128 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 128, false>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       nullptr);
   else if (d == 128 && block == 64)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 64, false>), grid, dim3(128), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       nullptr);
   else if (d == 64 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 128, false>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       nullptr);
   else
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 64, false>), grid, dim3(128), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H);
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       nullptr);
 }
 
 void launch_sparse_attention_f32(const float* q, const float* k,
@@ -665,32 +741,44 @@ void launch_sparse_attention_f32(const float* q, const float* k,
 }
 
 // Dense rows of the protected tokens (Eq. (11) first case), written over O
-// and lse: the gather variants, blocks of 128 gathered rows, no workspace.
+// and lse: the gather variants, blocks of 128 gathered rows; with more than
+// one key split the partials go to ws and token_combine_kernel writes O/lse.
 void launch_protected_token_attention_bf16(const uint16_t* q, const uint16_t* k,
                                            const uint16_t* v, uint16_t* o, float* lse,
                                            int B, int H, int L, int d, float scale,
-                                           const int32_t* tok_idx, int k_tok,
+                                           const int32_t* tok_idx, int k_tok, char* ws,
                                            hipStream_t s) {
-  constexpr int kRowBlock = 128;
-  const int n_b = ceil_div(L, kRowBlock);
+  const int n_b = ceil_div(L, kTokRowBlock);
   const int P = B * H;
   const float c = scale * kLog2e;
-  const dim3 grid(P * ceil_div(k_tok, kRowBlock));
+  const int ns = token_attn_splits(P, k_tok, n_b);
+  float* part = ns > 1 ? reinterpret_cast<float*>(ws) : nullptr;
+  const dim3 grid(P * ceil_div(k_tok, kTokRowBlock) * ns);
   if (d == 128)
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, kRowBlock, true>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
-                       k_tok, H);
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, kTokRowBlock, true>), grid, dim3(256), 0,
+                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
+                       k_tok, H, ns, part);
   else
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, kRowBlock, true>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
-                       k_tok, H);
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, kTokRowBlock, true>), grid, dim3(256), 0,
+                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
+                       k_tok, H, ns, part);
+  if (ns > 1) {
+    const size_t threads = static_cast<size_t>(P) * k_tok * (d / 4);
+    const dim3 cgrid(static_cast<unsigned>((threads + 255) / 256));
+    if (d == 128)
+      hipLaunchKernelGGL(token_combine_kernel<128>, cgrid, dim3(256), 0, s, part, ns, P, L, H,
+                         tok_idx, k_tok, o, lse);
+    else
+      hipLaunchKernelGGL(token_combine_kernel<64>, cgrid, dim3(256), 0, s, part, ns, P, L, H,
+                         tok_idx, k_tok, o, lse);
+  }
 }
 
 void launch_protected_token_attention_f32(const float* q, const float* k, const float* v,
                                           float* o, float* lse, int B, int H, int L, int d,
                                           float scale, const int32_t* tok_idx, int k_tok,
                                           hipStream_t s) {
-  constexpr int kRowBlock = 128;
+  constexpr int kRowBlock = kTokRowBlock;
   const int n_b = ceil_div(L, kRowBlock);
   const dim3 grid(ceil_div(k_tok, kRowBlock), B * H);
   if (d == 128)

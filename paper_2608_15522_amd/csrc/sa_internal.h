@@ -100,10 +100,41 @@ void launch_saliency_ema(float* s_bar, const float* s, size_t n, float alpha,
                          hipStream_t st);
 void launch_select_protected_tokens(const float* sal_tok, int B, int L, int k_tok,
                                     int32_t* tok_idx, uint8_t* tok_flag, hipStream_t st);
+// Protected-token rows run in workgroups of kTokRowBlock gathered rows.  The
+// keys of a row are cut into n_split runs so that the launch fills the 512
+// workgroup slots of the chip (256 CUs, 2 attention workgroups each) in
+// whole rounds: n_split minimises rounds/n_split * (1 + 0.02*n_split), where
+// the second factor prices each workgroup's fixed cost (pipeline fill, the
+// partial row, its share of the combine); 1 <= n_split <= 8, and every run
+// keeps at least 4 key blocks.
+constexpr int kTokRowBlock = 128;
+inline int token_attn_splits(int P, int k_tok, int n_b) {
+  const long units = static_cast<long>(P) * ceil_div(k_tok, kTokRowBlock);
+  int smax = n_b / 4;
+  smax = smax < 1 ? 1 : (smax > 8 ? 8 : smax);
+  int best = 1;
+  double best_cost = 0.0;
+  for (int s = 1; s <= smax; ++s) {
+    const double rounds = static_cast<double>((units * s + 511) / 512);
+    const double cost = rounds / s * (1.0 + 0.02 * s);
+    if (s == 1 || cost < best_cost - 1e-9) {
+      best = s;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+// Partial rows [n_split][B*H][k_tok][d] f32, then (m, l) [n_split][B*H][k_tok]
+// float2; none with one split.
+inline size_t token_attn_ws_bytes(int B, int H, int L, int d, int k_tok) {
+  const int ns = token_attn_splits(B * H, k_tok, ceil_div(L, kTokRowBlock));
+  if (ns <= 1 || k_tok <= 0) return 0;
+  return align_up(static_cast<size_t>(ns) * B * H * k_tok * (static_cast<size_t>(d) * 4 + 8));
+}
 void launch_protected_token_attention_bf16(const uint16_t* q, const uint16_t* k,
                                            const uint16_t* v, uint16_t* o, float* lse,
                                            int B, int H, int L, int d, float scale,
-                                           const int32_t* tok_idx, int k_tok,
+                                           const int32_t* tok_idx, int k_tok, char* ws,
                                            hipStream_t s);
 void launch_protected_token_attention_f32(const float* q, const float* k, const float* v,
                                           float* o, float* lse, int B, int H, int L, int d,

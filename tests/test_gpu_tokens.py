@@ -81,6 +81,12 @@ LAYERS = [
     ("bf16_d128_many_tokens", BASE.with_(name="t3", H=1, frames=3, rows=10, cols=15,
                                          L_a=32, n_plant=1), 2, 0.6),
     ("f32_tiny", synth.WORKLOADS["tiny_f32"], 4, 0.1),
+    # 16 key blocks of 128 with an 80-key tail: the keys of a row go to 4 runs
+    ("bf16_d128_split4", BASE.with_(name="t4", H=2, frames=4, rows=10, cols=50, L_a=64,
+                                    n_plant=2), 3, 0.05),
+    # 11 key blocks of 128: two runs of 5 and 6 blocks
+    ("bf16_d64_split2", BASE.with_(name="t5", H=3, d=64, block=64, frames=2, rows=10,
+                                   cols=65, L_a=40, n_plant=1), 4, 0.1),
 ]
 
 
@@ -155,3 +161,34 @@ def test_token_protected_layer_fullsize_ovi():
     print("ovi tokens", dict(o_err=o_err, lse_err=l_err), flush=True)
     assert o_err <= TOL_O["bf16"] and l_err <= TOL_LSE["bf16"]
     assert np.all(np.isfinite(g["o"]))
+
+
+def test_split_rows_skip_out_of_range_entries():
+    """With the keys of each row split into runs, entries of tok_idx outside
+    [0, L) leave O and lse alone and the other rows are the dense rows."""
+    w = BASE.with_(name="t6", H=2, frames=4, rows=10, cols=50, L_a=64, n_plant=1)
+    L = w.L_v
+    assert sa.sa_workspace_size(sa.SA_CALL_TOKEN_ATTENTION, w.B, w.H, L, 6, w.d, 0) > 0
+    x = synth.make_inputs(w)
+    t = {kk: to_dev(x[kk], w.dtype) for kk in ("q_v", "k_v", "v_v")}
+    idx = torch.tensor([[3, -1, 17, L, 400, L - 1]], dtype=torch.int32, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(1)
+    o = torch.randn(t["q_v"].shape, device="cuda", generator=g).to(torch.bfloat16)
+    lse = torch.randn(w.B, w.H, L, device="cuda", generator=g)
+    o0, lse0 = o.clone(), lse.clone()
+    sa.sa_protected_token_attention(t["q_v"], t["k_v"], t["v_v"], w.scale, idx, o, lse)
+    torch.cuda.synchronize()
+    o, lse, o0, lse0 = (a.float().cpu().numpy() for a in (o, lse, o0, lse0))
+    valid = [0, 2, 4, 5]
+    tok = idx.cpu().numpy()
+    rows = [(0, h, j) for h in range(w.H) for j in valid]
+    O_ref, lse_ref = oracle.token_protected_rows(x["q_v"], x["k_v"], x["v_v"], w.scale,
+                                                 tok, rows)
+    for (b, h, j) in rows:
+        r = tok[b, j]
+        assert float(np.abs(o[b, h, r] - O_ref[(b, h, j)]).max()) <= TOL_O["bf16"]
+        assert abs(float(lse[b, h, r]) - lse_ref[(b, h, j)]) <= TOL_LSE["bf16"]
+    other = np.ones(L, dtype=bool)
+    other[tok[0, valid]] = False
+    assert np.array_equal(o[:, :, other], o0[:, :, other])
+    assert np.array_equal(lse[:, :, other], lse0[:, :, other])

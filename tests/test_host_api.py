@@ -71,6 +71,36 @@ def test_workspace_sizes():
     assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 0, 0, 10, 0, 0, 0) == 0
 
 
+def _splits(P, k_tok, n_b):
+    """The key-split rule of the protected-token rows, restated."""
+    units = P * -(-k_tok // 128)
+    smax = min(8, max(1, n_b // 4))
+    costs = [(-(-units * s // 512)) / s * (1 + 0.02 * s) for s in range(1, smax + 1)]
+    return 1 + min(range(len(costs)), key=lambda i: (costs[i] - 1e-9 * (i == 0), i))
+
+
+@pytest.mark.parametrize("B,H,L,k_tok,d,splits", [
+    (1, 24, 32760, 1638, 128, 3),   # Ovi-like, 5 % of the tokens: 312 row blocks
+    (1, 1, 1000, 10, 128, 2),       # one row block, 8 key blocks
+    (1, 24, 32760, 100, 64, 8),     # 24 row blocks
+    (2, 24, 75600, 3780, 128, 1),   # 1440 row blocks fill the chip
+    (1, 1, 300, 5, 64, 1),          # 3 key blocks: no split
+])
+def test_token_attention_workspace(B, H, L, k_tok, d, splits):
+    """Partial rows (d f32 + m, l) per split, none without a split."""
+    assert _splits(B * H, k_tok, -(-L // 128)) == splits
+    need = sa.sa_workspace_size(sa.SA_CALL_TOKEN_ATTENTION, B, H, L, k_tok, d, 0)
+    want = 0 if splits == 1 else (splits * B * H * k_tok * (4 * d + 8) + 255) // 256 * 256
+    assert need == want
+
+
+def test_token_attention_workspace_rejects():
+    for bad in [(0, 1, 10, 1, 64, 0), (1, 1, 10, 11, 64, 0), (1, 1, 10, -1, 64, 0),
+                (1, 1, 10, 1, 96, 0)]:
+        assert sa.sa_workspace_size(sa.SA_CALL_TOKEN_ATTENTION, *bad) == 0
+    assert sa.sa_workspace_size(sa.SA_CALL_TOKEN_ATTENTION, 1, 24, 32760, 0, 128, 0) == 0
+
+
 def _attn(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
              dtype=0, scale=0.088, block=128, kv_idx=FAKE, kv_cnt=FAKE, ws=FAKE,
@@ -118,7 +148,8 @@ def _tokens(**kw):
 
 def _ptok(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
-             dtype=0, scale=0.088, tok_idx=FAKE, k_tok=10, stream=None)
+             dtype=0, scale=0.088, tok_idx=FAKE, k_tok=10, ws=FAKE, ws_bytes=1 << 40,
+             stream=None)
     a.update(kw)
     return sa.lib().sa_protected_token_attention(*a.values())
 
@@ -166,6 +197,8 @@ def _cache(**kw):
     (_ptok, dict(tok_idx=None), sa.SA_ERR_INVALID_ARG, "tok_idx is NULL"),
     (_ptok, dict(o=None), sa.SA_ERR_INVALID_ARG, "o is NULL"),
     (_ptok, dict(scale=-1.0), sa.SA_ERR_INVALID_ARG, "scale"),
+    (_ptok, dict(ws_bytes=4), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_ptok, dict(ws=None), sa.SA_ERR_INVALID_ARG, "ws is NULL"),
     (_attn, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
     (_attn, dict(block=32), sa.SA_ERR_UNSUPPORTED, "block"),
     (_attn, dict(dtype=7), sa.SA_ERR_UNSUPPORTED, "dtype"),
