@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-ATTN_KERNEL = "sparse_attn_bf16_kernel<128,128>"
+ATTN_KERNEL = "sparse_attn_bf16_kernel<128,128,false>"
 ATTN_SOURCES = ("paper_2608_15522_amd/csrc/sa_attn.hip",
                 "paper_2608_15522_amd/csrc/sa_device.h")
 TRAFFIC_FILE = "profiles/ovi_layer_hbm_bytes.md"
@@ -398,7 +398,7 @@ def main():
             "per_call_ms": {k: round(v, 4) for k, v in pc_tok.items()},
             "sparse_tflop": round(computed_flops(kvi_tok, kvc_tok, w.L_v, w.block, w.d) / 1e12, 4),
             "dense_rows_tflop": round(rows_flops / 1e12, 4),
-            "dense_rows_kernel": "sparse_attn_bf16_kernel<128,128,gather>",
+            "dense_rows_kernels": "sparse_attn_bf16_kernel<128,128,true> + token_combine_kernel<128>",
             "dense_rows_tflops": round(rows_tf, 2),
             "dense_rows_frac_of_peak": round(rows_tf / PEAK_BF16_TFLOPS, 4)}
     if not args.no_cache_indicator:
