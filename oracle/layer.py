@@ -11,6 +11,7 @@ from .saliency import cross_scores, token_to_block_saliency
 from .selection import select_protected
 from .mask import block_mask
 from .attention import masked_attention
+from .tokens import select_protected_tokens, token_protected_attention
 
 
 def protected_sparse_layer(q_v, k_v, v_v, q_a, k_a, scale, block, k_keep,
@@ -28,6 +29,24 @@ def protected_sparse_layer(q_v, k_v, v_v, q_a, k_a, scale, block, k_keep,
     return {"sal_v_tok": s_v, "sal_v_blk": s_blk, "sal_a_tok": s_a,
             "prot_idx": prot_idx, "prot_flag": prot_flag, **m,
             "O": O, "lse": lse}
+
+
+def modality_protected_layer(q, k, v, sal_bar, scale, block, k_keep, k_tok):
+    """Protected sparse self-attention of one modality m in {v, a}
+    (Sec. 4.2, Eq. (8)-(11)).
+
+    The protected query tokens P^m are the top ``k_tok`` = ceil(rho_m N_m)
+    tokens of the lagged saliency map ``sal_bar`` [B, N_m] (Eq. (8), ties to
+    the lower index); the sparse pattern S_m is the pooled-QK block top-k of
+    the modality's own Q and K (Eq. (6)) with no block protection; a
+    protected query keeps every key (Eq. (9)), any other query the key blocks
+    of its query block (Eq. (11)).  For the audio branch ``sal_bar`` is the
+    audio-token saliency of the v->a direction (Sec. 4.1)."""
+    tok_idx, tok_flag = select_protected_tokens(sal_bar, k_tok)
+    m = block_mask(q, k, scale, block, k_keep, None)
+    O, lse = token_protected_attention(q, k, v, scale, block, m["kv_idx"],
+                                       m["kv_cnt"], tok_flag)
+    return {"tok_idx": tok_idx, "tok_flag": tok_flag, **m, "O": O, "lse": lse}
 
 
 def computed_flops(kv_idx, kv_cnt, N, block, d):

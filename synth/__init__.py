@@ -67,6 +67,8 @@ class Workload:
     prescale: bool      # multiply Q/K/V by 1/sqrt(d) before planting
     k_prot_fixed: int = -1
     seed: int = 0
+    block_a: int = 64   # audio branch: tokens per block of its sparse pattern
+    rho_a: float = 0.05  # audio branch: protected token ratio
 
     @property
     def L_v(self) -> int:
@@ -90,6 +92,20 @@ class Workload:
         if self.k_prot_fixed >= 0:
             return self.k_prot_fixed
         return budget(self.rho, self.n_b)
+
+    @property
+    def n_b_a(self) -> int:
+        return -(-self.L_a // self.block_a)
+
+    @property
+    def k_keep_a(self) -> int:
+        """Audio key blocks kept per non-protected audio query block (the
+        video keep ratio over the audio blocks)."""
+        return budget(self.density, self.n_b_a)
+
+    @property
+    def k_tok_a(self) -> int:
+        return budget(self.rho_a, self.L_a)
 
     @property
     def scale(self) -> float:
@@ -215,3 +231,21 @@ def make_inputs(w: Workload, seed: int | None = None, with_v: bool = True):
     elif w.dtype != "f32":
         raise ValueError(f"unknown dtype {w.dtype!r}")
     return out
+
+
+def make_audio_values(w: Workload, seed: int | None = None) -> np.ndarray:
+    """V^a [B, H, L_a, d] for the audio branch's self-attention, standard
+    normal from its own generator (seeded with (seed, 1)) so that the draws
+    of ``make_inputs`` do not change; scaled and rounded like the other
+    inputs of ``w``."""
+    seed = w.seed if seed is None else seed
+    rng = np.random.default_rng([seed, 1])
+    arr = np.empty((w.B, w.H, w.L_a, w.d), dtype=np.float32)
+    for b in range(w.B):
+        for h in range(w.H):
+            rng.standard_normal(dtype=np.float32, out=arr[b, h])
+    if w.prescale:
+        arr *= np.float32(1.0 / math.sqrt(w.d))
+    if w.dtype == "bf16":
+        arr = round_to_bf16(arr).reshape(arr.shape)
+    return arr
