@@ -59,6 +59,8 @@ def parse():
                    help="lagged-saliency weight alpha of Eq. (4) in that run")
     p.add_argument("--no-cache-indicator", action="store_true",
                    help="skip timing the cache-reuse indicator")
+    p.add_argument("--no-audio-branch", action="store_true",
+                   help="skip timing the audio branch's protected sparse attention")
     p.add_argument("--sweep", default=None,
                    help="also run the density x protection sweep, one JSON "
                         "line per cell appended to this file")
@@ -181,6 +183,66 @@ def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
     per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
                 for j, n in enumerate(names)}
     return wall * 1e3 / steps, per_call, kv_idx.cpu().numpy(), kv_cnt.cpu().numpy()
+
+
+def time_audio_branch(plan, t, w, steps, warmup, torch, sa):
+    """The audio branch's protected sparse self-attention (Eq. (8)-(11),
+    m = a) at the workload's audio shape, on the audio-token saliency of the
+    layer's cross scores: lagged update, protected audio tokens, the audio
+    block pattern, block-sparse attention and the dense rows.  V^a is drawn
+    on the device.  Returns (ms per branch, per-call ms, computed flops)."""
+    dev = t["q_a"].device
+    g = torch.Generator(device="cuda").manual_seed(1)
+    v_a = torch.randn(t["q_a"].shape, device=dev, generator=g).to(t["q_a"].dtype)
+    plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+    sal_bar = plan.sal_a_tok.clone()
+    n_b, k_tok = w.n_b_a, w.k_tok_a
+    tok_idx = torch.empty(w.B, k_tok, dtype=torch.int32, device=dev)
+    kv_idx = torch.empty(w.B, w.H, n_b, n_b, dtype=torch.int32, device=dev)
+    kv_cnt = torch.empty(w.B, w.H, n_b, dtype=torch.int32, device=dev)
+    o = torch.empty_like(t["q_a"])
+
+    def ws(call, la):
+        return torch.empty(max(1, sa.sa_workspace_size(call, w.B, w.H, w.L_a, la, w.d,
+                                                       w.block_a)),
+                           dtype=torch.uint8, device=dev)
+    ws_mask = ws(sa.SA_CALL_BUILD_BLOCK_MASK, 1)
+    ws_attn = ws(sa.SA_CALL_SPARSE_ATTENTION, 1)
+    ws_tok = ws(sa.SA_CALL_TOKEN_ATTENTION, k_tok)
+    names = ["sa_saliency_ema", "sa_select_protected_tokens", "sa_build_block_mask",
+             "sa_sparse_attention", "sa_protected_token_attention"]
+
+    def step(e=None):
+        rec = (lambda j: e[j].record()) if e else (lambda j: None)
+        rec(0)
+        sa.sa_saliency_ema(sal_bar, plan.sal_a_tok, 0.5)
+        rec(1)
+        sa.sa_select_protected_tokens(sal_bar, k_tok, tok_idx=tok_idx, want_flag=False)
+        rec(2)
+        sa.sa_build_block_mask(t["q_a"], t["k_a"], plan.scale, w.block_a, w.k_keep_a, None,
+                               kv_idx=kv_idx, kv_cnt=kv_cnt, ws=ws_mask)
+        rec(3)
+        sa.sa_sparse_attention(t["q_a"], t["k_a"], v_a, plan.scale, w.block_a, kv_idx,
+                               kv_cnt, o=o, ws=ws_attn)
+        rec(4)
+        sa.sa_protected_token_attention(t["q_a"], t["k_a"], v_a, plan.scale, tok_idx, o,
+                                        ws=ws_tok)
+        rec(5)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
+                for j, n in enumerate(names)}
+    flops = (computed_flops(kv_idx.cpu().numpy(), kv_cnt.cpu().numpy(), w.L_a, w.block_a, w.d)
+             + 4.0 * w.d * k_tok * w.L_a * w.B * w.H)
+    return wall * 1e3 / steps, per_call, flops
 
 
 def time_cache_indicator(w, steps, torch, sa):
@@ -401,6 +463,14 @@ def main():
             "dense_rows_kernels": "sparse_attn_bf16_kernel<128,128,true> + token_combine_kernel<128>",
             "dense_rows_tflops": round(rows_tf, 2),
             "dense_rows_frac_of_peak": round(rows_tf / PEAK_BF16_TFLOPS, 4)}
+    if not args.no_audio_branch:
+        ms_a, pc_a, flops_a = time_audio_branch(plan, t, w, args.steps, args.warmup, torch, sa)
+        dense_a = 4.0 * w.B * w.H * w.L_a ** 2 * w.d
+        res["audio_branch"] = {
+            "L_a": w.L_a, "block_a": w.block_a, "k_keep_a": w.k_keep_a, "k_tok_a": w.k_tok_a,
+            "ms": round(ms_a, 4), "per_call_ms": {k: round(v, 4) for k, v in pc_a.items()},
+            "computed_tflop": round(flops_a / 1e12, 5),
+            "effective_dense_tflops": round(dense_a / (ms_a * 1e-3) / 1e12, 2)}
     if not args.no_cache_indicator:
         ci_ms, ci_bytes = time_cache_indicator(w, args.steps, torch, sa)
         ci_gbs = ci_bytes / (ci_ms * 1e-3) / 1e9
