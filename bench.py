@@ -59,6 +59,10 @@ def parse():
                    help="lagged-saliency weight alpha of Eq. (4) in that run")
     p.add_argument("--no-cache-indicator", action="store_true",
                    help="skip timing the cache-reuse indicator")
+    p.add_argument("--error-by-rank", action="store_true",
+                   help="also report the attention error of vanilla, block-protected and "
+                        "token-protected sparse attention against the dense run, by the "
+                        "tokens' saliency rank")
     p.add_argument("--no-audio-branch", action="store_true",
                    help="skip timing the audio branch's protected sparse attention")
     p.add_argument("--sweep", default=None,
@@ -243,6 +247,55 @@ def time_audio_branch(plan, t, w, steps, warmup, torch, sa):
     flops = (computed_flops(kv_idx.cpu().numpy(), kv_cnt.cpu().numpy(), w.L_a, w.block_a, w.d)
              + 4.0 * w.d * k_tok * w.L_a * w.B * w.H)
     return wall * 1e3 / steps, per_call, flops
+
+
+def error_by_rank(plan, t, w, x, di, dc, k_tok, torch, sa):
+    """A synthetic analogue of the paper's Fig. 4: the error of vanilla
+    sparse attention, block protection and token protection against the
+    dense run (every list full), per video token, against the token's rank
+    in the a->v saliency.  All outputs come from the library; the error of a
+    token is ||O_x - O_dense||_2 averaged over heads, divided by the mean of
+    ||O_dense||_2 over all (head, token) rows (one global scale: the dense
+    rows of near-uniform attention have tiny norms, which makes per-row
+    relative errors meaningless).  Returns the report dict."""
+    B, H, L = w.B, w.H, w.L_v
+    plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+    sal = plan.sal_v_tok.clone()
+    o_dense, _ = sa.sa_sparse_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, w.block,
+                                        di, dc, ws=plan.ws)
+    o_dense = o_dense.float()
+    kv_idx, kv_cnt, _, _ = sa.sa_build_block_mask(t["q_v"], t["k_v"], plan.scale, w.block,
+                                                  w.k_keep, None, ws=plan.ws)
+    o_van, _ = sa.sa_sparse_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, w.block,
+                                      kv_idx, kv_cnt, ws=plan.ws)
+    tok_idx, tok_flag = sa.sa_select_protected_tokens(sal, k_tok)
+    o_tok = o_van.clone()
+    sa.sa_protected_token_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, tok_idx, o_tok)
+    plan.select_protected()
+    plan.build_block_mask(t["q_v"], t["k_v"])
+    o_blk, _ = sa.sa_sparse_attention(t["q_v"], t["k_v"], t["v_v"], plan.scale, w.block,
+                                      plan.kv_idx, plan.kv_cnt, ws=plan.ws)
+    torch.cuda.synchronize()
+    scale = float(o_dense.norm(dim=-1).mean())
+
+    def err(o):
+        return (o.float() - o_dense).norm(dim=-1).mean(dim=1) / scale  # [B, L]
+
+    errs = {"vanilla": err(o_van), "block_protected": err(o_blk),
+            "token_protected": err(o_tok)}
+    rank = torch.argsort(torch.argsort(-sal, dim=1, stable=True), dim=1).float() / L
+    edges = [0.0, 0.01, 0.05, 0.10, 0.25, 0.50, 1.0001]
+    bins = []
+    for lo, hi in zip(edges[:-1], edges[1:]):
+        sel = (rank >= lo) & (rank < hi)
+        bins.append({"rank_pct": f"{lo * 100:g}-{min(hi, 1.0) * 100:g}",
+                     **{k: round(float(v[sel].mean()), 5) for k, v in errs.items()}})
+    planted = torch.from_numpy(x["planted"]).cuda()
+    return {"k_keep": w.k_keep, "k_prot_blocks": w.k_prot, "k_tok": k_tok,
+            "metric": "per token: mean over heads of ||O - O_dense||_2, over the mean ||O_dense||_2",
+            "by_saliency_rank": bins,
+            "planted_tokens": {k: round(float(v[planted].mean()), 5) for k, v in errs.items()},
+            "other_tokens": {k: round(float(v[~planted].mean()), 5) for k, v in errs.items()}}
 
 
 def time_cache_indicator(w, steps, torch, sa):
@@ -463,6 +516,9 @@ def main():
             "dense_rows_kernels": "sparse_attn_bf16_kernel<128,128,true> + token_combine_kernel<128>",
             "dense_rows_tflops": round(rows_tf, 2),
             "dense_rows_frac_of_peak": round(rows_tf / PEAK_BF16_TFLOPS, 4)}
+    if args.error_by_rank:
+        res["error_by_rank"] = error_by_rank(plan, t, w, x, di, dc, synth.budget(w.rho, w.L_v),
+                                             torch, sa)
     if not args.no_audio_branch:
         ms_a, pc_a, flops_a = time_audio_branch(plan, t, w, args.steps, args.warmup, torch, sa)
         dense_a = 4.0 * w.B * w.H * w.L_a ** 2 * w.d
