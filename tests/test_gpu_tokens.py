@@ -41,9 +41,12 @@ def test_saliency_ema_in_place_is_a_fixed_point():
 
 
 # ------------------------------------------------------- Eq. (8), token level
-SELECT = [(1, 1, 0), (1, 1, 1), (2, 5, 3), (1, 1000, 50), (2, 1000, 1000),
-          (1, 1000, 0), (1, 32760, 1638), (1, 32768, 4000), (1, 32769, 1639),
-          (2, 75600, 3780)]
+# one wave up to L = 512 and up to 2048; 16 waves with 4, 16 or 32 register
+# keys per lane, or keys read from memory beyond L = 32768
+SELECT = [(1, 1, 0), (1, 1, 1), (2, 5, 3), (1, 512, 26), (1, 513, 26), (1, 1000, 50),
+          (2, 1000, 1000), (1, 1000, 0), (1, 2048, 103), (1, 2049, 103), (1, 4096, 205),
+          (3, 16384, 820), (1, 16385, 5000), (1, 32760, 1638), (1, 32768, 4000),
+          (1, 32769, 1639), (2, 75600, 3780)]
 
 
 @pytest.mark.parametrize("B,L,k", SELECT)
