@@ -22,8 +22,9 @@ Sparse Attention"):
 * ``cache``      -- Eq. (12)-(15): the synchronization-aware cache-reuse
   indicator (relative L1 changes, protected-row change, saliency drift);
 * ``layer``      -- the steps composed: the video layer with protected blocks,
-  and token-protected sparse self-attention of either modality (Eq. (8)-(11),
-  m in {v, a}; the audio branch with the audio-token saliency).
+  token-protected sparse self-attention of either modality (Eq. (8)-(11),
+  m in {v, a}; the audio branch with the audio-token saliency), and the two
+  cross-modal attention forwards with the saliency of their softmax.
 
 Where the paper is silent or ambiguous the reading taken is stated in the
 function that depends on it.  Parity status: every public function here is
@@ -35,8 +36,8 @@ from .selection import topk_order, select_protected
 from .mask import block_pool, pooled_scores, block_mask, kv_lists_from_mask
 from .attention import (dense_attention, masked_attention,
                         additive_mask_attention, key_tokens_of_row)
-from .layer import (protected_sparse_layer, modality_protected_layer, computed_flops,
-                    dense_flops)
+from .layer import (protected_sparse_layer, modality_protected_layer,
+                    cross_attention_with_saliency, computed_flops, dense_flops)
 from .tokens import (saliency_ema, select_protected_tokens,
                      token_protected_attention, token_protected_rows)
 from .cache import relative_l1, saliency_drift, cache_indicator
@@ -46,7 +47,7 @@ __all__ = [
     "select_protected", "block_pool", "pooled_scores", "block_mask",
     "kv_lists_from_mask", "dense_attention", "masked_attention",
     "additive_mask_attention", "key_tokens_of_row", "protected_sparse_layer",
-    "modality_protected_layer",
+    "modality_protected_layer", "cross_attention_with_saliency",
     "computed_flops", "dense_flops", "saliency_ema", "select_protected_tokens",
     "token_protected_attention", "token_protected_rows", "relative_l1",
     "saliency_drift", "cache_indicator",

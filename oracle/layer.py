@@ -10,7 +10,7 @@ import numpy as np
 from .saliency import cross_scores, token_to_block_saliency
 from .selection import select_protected
 from .mask import block_mask
-from .attention import masked_attention
+from .attention import dense_attention, masked_attention
 from .tokens import select_protected_tokens, token_protected_attention
 
 
@@ -47,6 +47,19 @@ def modality_protected_layer(q, k, v, sal_bar, scale, block, k_keep, k_tok):
     O, lse = token_protected_attention(q, k, v, scale, block, m["kv_idx"],
                                        m["kv_cnt"], tok_flag)
     return {"tok_idx": tok_idx, "tok_flag": tok_flag, **m, "O": O, "lse": lse}
+
+
+def cross_attention_with_saliency(q_a, k_a, v_a, q_v, k_v, v_v, scale):
+    """The two cross-modal attention forwards of a layer and the saliency of
+    Eq. (1)-(2) taken from the same softmax: O^a = softmax(Q^a (K^v)^T s) V^v
+    and O^v = softmax(Q^v (K^a)^T s) V^a with their row log-sum-exps, and
+    (s_v, s_a) the column masses of those two softmax matrices, summed over
+    queries and heads and divided by H*L_a and H*L_v.  Returns a dict."""
+    O_a, lse_a = dense_attention(q_a, k_v, v_v, scale)
+    O_v, lse_v = dense_attention(q_v, k_a, v_a, scale)
+    s_v, s_a = cross_scores(q_a, k_v, scale, q_v, k_a)
+    return {"O_a": O_a, "lse_a": lse_a, "O_v": O_v, "lse_v": lse_v,
+            "sal_v_tok": s_v, "sal_a_tok": s_a}
 
 
 def computed_flops(kv_idx, kv_cnt, N, block, d):
