@@ -63,6 +63,9 @@ def parse():
                    help="also report the attention error of vanilla, block-protected and "
                         "token-protected sparse attention against the dense run, by the "
                         "tokens' saliency rank")
+    p.add_argument("--no-cross-attention", action="store_true",
+                   help="skip timing the cross-modal attention forwards and the saliency "
+                        "from their LSEs")
     p.add_argument("--no-audio-branch", action="store_true",
                    help="skip timing the audio branch's protected sparse attention")
     p.add_argument("--sweep", default=None,
@@ -298,6 +301,62 @@ def error_by_rank(plan, t, w, x, di, dc, k_tok, torch, sa):
             "other_tokens": {k: round(float(v[~planted].mean()), 5) for k, v in errs.items()}}
 
 
+def time_cross_attention(plan, t, w, steps, warmup, torch, sa):
+    """The two cross-modal attention forwards (a->v: Q^a over K^v, V^v; v->a:
+    Q^v over K^a, V^a) with their row LSEs, then the saliency of both
+    directions from those LSEs (sa_cross_scores_from_lse), against the
+    standalone saliency call.  V^a is drawn on the device.  Returns the
+    report dict."""
+    dev = t["q_a"].device
+    g = torch.Generator(device="cuda").manual_seed(2)
+    v_a = torch.randn(t["k_a"].shape, device=dev, generator=g).to(t["k_a"].dtype)
+    B, H, L_v, L_a, d = w.B, w.H, w.L_v, w.L_a, w.d
+    o_a = torch.empty_like(t["q_a"])
+    o_v = torch.empty_like(t["q_v"])
+    lse_a = torch.empty(B, H, L_a, dtype=torch.float32, device=dev)
+    lse_v = torch.empty(B, H, L_v, dtype=torch.float32, device=dev)
+
+    def ws(Lq, Lk):
+        return torch.empty(max(1, sa.sa_workspace_size(sa.SA_CALL_CROSS_ATTENTION, B, H, Lq, Lk,
+                                                       d, 0)), dtype=torch.uint8, device=dev)
+    ws_a, ws_v = ws(L_a, L_v), ws(L_v, L_a)
+    names = ["a2v_forward", "v2a_forward", "sa_cross_scores_from_lse", "sa_cross_scores"]
+
+    def step(e=None):
+        rec = (lambda j: e[j].record()) if e else (lambda j: None)
+        rec(0)
+        sa.sa_cross_attention(t["q_a"], t["k_v"], t["v_v"], plan.scale, o=o_a, lse=lse_a,
+                              ws=ws_a)
+        rec(1)
+        sa.sa_cross_attention(t["q_v"], t["k_a"], v_a, plan.scale, o=o_v, lse=lse_v, ws=ws_v)
+        rec(2)
+        sa.sa_cross_scores_from_lse(t["q_a"], t["k_v"], t["q_v"], t["k_a"], lse_a, lse_v,
+                                    plan.scale, w.block, sal_v_tok=plan.sal_v_tok,
+                                    sal_v_blk=plan.sal_v_blk, sal_a_tok=plan.sal_a_tok,
+                                    ws=plan.ws)
+        rec(3)
+        plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        rec(4)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    for i in range(steps):
+        step(ev[i])
+    torch.cuda.synchronize()
+    ms = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
+          for j, n in enumerate(names)}
+    flops = 4.0 * B * H * L_a * L_v * d  # each direction
+    fwd_ms = ms["a2v_forward"] + ms["v2a_forward"]
+    return {"per_call_ms": {k: round(v, 4) for k, v in ms.items()},
+            "forward_tflop_each": round(flops / 1e12, 4),
+            "a2v_forward_tflops": round(flops / (ms["a2v_forward"] * 1e-3) / 1e12, 1),
+            "v2a_forward_tflops": round(flops / (ms["v2a_forward"] * 1e-3) / 1e12, 1),
+            "forwards_plus_saliency_ms": round(fwd_ms + ms["sa_cross_scores_from_lse"], 4),
+            "forwards_plus_standalone_saliency_ms": round(fwd_ms + ms["sa_cross_scores"], 4)}
+
+
 def time_cache_indicator(w, steps, torch, sa):
     """The cache-reuse indicator (Eq. (12)-(15)) on block outputs of the
     workload's size (C = H*d channels per token, its dtype): current and
@@ -519,6 +578,9 @@ def main():
     if args.error_by_rank:
         res["error_by_rank"] = error_by_rank(plan, t, w, x, di, dc, synth.budget(w.rho, w.L_v),
                                              torch, sa)
+    if not args.no_cross_attention:
+        res["cross_attention"] = time_cross_attention(plan, t, w, args.steps, args.warmup,
+                                                      torch, sa)
     if not args.no_audio_branch:
         ms_a, pc_a, flops_a = time_audio_branch(plan, t, w, args.steps, args.warmup, torch, sa)
         dense_a = 4.0 * w.B * w.H * w.L_a ** 2 * w.d

@@ -22,8 +22,11 @@
  *                                      token saliency (Eq. (3)/(8));
  *   7. sa_protected_token_attention -- dense rows of the protected tokens
  *                                      over the sparse output (Eq. (9)-(11));
+ * the cross-modal attention forward whose row LSEs give the saliency:
+ *   8. sa_cross_attention           -- dense cross-modal attention (Eq. (1));
+ *   9. sa_cross_scores_from_lse     -- the saliency from its row LSEs;
  * and the cache-reuse decision:
- *   8. sa_cache_indicator           -- synchronization-aware cache-reuse
+ *  10. sa_cache_indicator           -- synchronization-aware cache-reuse
  *                                      indicator (Sec. 4.3, Eq. (12)-(15)).
  *
  * Conventions shared by every call
@@ -72,7 +75,8 @@ enum {
   SA_CALL_SPARSE_ATTENTION = 2,
   SA_CALL_SELECT_PROTECTED = 3,
   SA_CALL_CACHE_INDICATOR = 4,
-  SA_CALL_TOKEN_ATTENTION = 5
+  SA_CALL_TOKEN_ATTENTION = 5,
+  SA_CALL_CROSS_ATTENTION = 6
 };
 
 /*
@@ -105,6 +109,55 @@ int sa_cross_scores(const void* q_a, const void* k_v, const void* q_v,
                     int dtype, float scale, int block, float* sal_v_tok,
                     float* sal_v_blk, float* sal_a_tok, int accumulate,
                     void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * sa_cross_attention -- the dense cross-modal attention forward of one layer
+ * (the a->v and v->a attention of Eq. (1) and the sentence after Eq. (2)),
+ * whose row log-sum-exps feed sa_cross_scores_from_lse.
+ *
+ * O = softmax(Q K^T * scale) V for every query of Q against all Lk keys:
+ * Q^a against K^v, V^v (Lq = L_a, Lk = L_v) for the a->v direction, Q^v
+ * against K^a, V^a (Lq = L_v, Lk = L_a) for v->a.  When Lq/128 row blocks
+ * per head leave the chip short of work, the keys of each row block are cut
+ * into up to 8 runs whose partial rows (f32) are merged in a fixed order.
+ *
+ *   q          [B,H,Lq,d] bf16; 1 <= Lq <= 262144
+ *   k, v       [B,H,Lk,d] bf16; 1 <= Lk <= 262144
+ *   o          [B,H,Lq,d] bf16 out (round to nearest even from fp32)
+ *   lse        [B,H,Lq] f32 out, natural log of the softmax denominator of
+ *              the scaled scores; nullable
+ *   dtype      SA_BF16 only (SA_F32 returns SA_ERR_UNSUPPORTED)
+ *   ws         workspace of at least sa_workspace_size(SA_CALL_CROSS_ATTENTION,
+ *              B, H, Lq, Lk, d, 0) bytes (0: ws may be NULL)
+ */
+int sa_cross_attention(const void* q, const void* k, const void* v, void* o,
+                       float* lse, int B, int H, int Lq, int Lk, int d,
+                       int dtype, float scale, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/*
+ * sa_cross_scores_from_lse -- sa_cross_scores's outputs, given the row
+ * log-sum-exps of the two cross-attention forwards (Sec. 4.1, Eq. (1)-(2)):
+ * the saliency as a side output of attention the model computes anyway.
+ *
+ * The softmax of Eq. (1) is exp(scale * q.k - lse) with lse the row LSE of
+ * that forward, so the first pass over the keys that sa_cross_scores needs
+ * for it is skipped in both directions.  Arguments as in sa_cross_scores,
+ * plus
+ *   lse_a      [B,H,L_a] f32: lse of sa_cross_attention(Q^a, K^v, V^v)
+ *   lse_v      [B,H,L_v] f32: lse of sa_cross_attention(Q^v, K^a, V^a);
+ *              NULL iff q_v is NULL
+ *   dtype      SA_BF16 only
+ *   ws         workspace of at least sa_workspace_size(SA_CALL_CROSS_SCORES)
+ * The results equal sa_cross_scores's up to the rounding of the given lse.
+ */
+int sa_cross_scores_from_lse(const void* q_a, const void* k_v, const void* q_v,
+                             const void* k_a, const float* lse_a,
+                             const float* lse_v, int B, int H, int L_v,
+                             int L_a, int d, int dtype, float scale, int block,
+                             float* sal_v_tok, float* sal_v_blk,
+                             float* sal_a_tok, int accumulate, void* ws,
+                             size_t ws_bytes, void* stream);
 
 /*
  * sa_select_protected -- protected query blocks (Sec. 4.2, Eq. (8), at block
@@ -271,7 +324,8 @@ int sa_cache_indicator(const void* y_v, const void* y_v_hat,
  * read by SA_CALL_CROSS_SCORES and SA_CALL_CACHE_INDICATOR (0 = no audio),
  * and SA_CALL_CACHE_INDICATOR reads B, L_v and L_a only.
  * SA_CALL_TOKEN_ATTENTION reads B, H, L_v (the sequence length L), d and
- * k_tok in the place of L_a; block is not read.  Returns 0 for sizes the
+ * k_tok in the place of L_a; SA_CALL_CROSS_ATTENTION reads B, H, Lq in the
+ * place of L_v, Lk in the place of L_a, and d; block is not read by either.  Returns 0 for sizes the
  * call rejects.
  * The figure covers both dtypes.
  */

@@ -11,6 +11,7 @@ from .binding import (  # noqa: F401
     sa_select_protected, sa_sparse_attention, sa_version, sa_workspace_size,
     sa_saliency_ema, sa_select_protected_tokens, sa_protected_token_attention,
     sa_cache_indicator, SA_CALL_CACHE_INDICATOR, SA_CALL_TOKEN_ATTENTION,
+    sa_cross_attention, sa_cross_scores_from_lse, SA_CALL_CROSS_ATTENTION,
     SA_BF16, SA_F32, SA_CALL_CROSS_SCORES, SA_CALL_BUILD_BLOCK_MASK,
     SA_CALL_SPARSE_ATTENTION, SA_CALL_SELECT_PROTECTED, SA_OK,
     SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP,

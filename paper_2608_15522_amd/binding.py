@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsa.so")
 SA_OK, SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP = range(5)
 SA_BF16, SA_F32 = 0, 1
 (SA_CALL_CROSS_SCORES, SA_CALL_BUILD_BLOCK_MASK, SA_CALL_SPARSE_ATTENTION,
- SA_CALL_SELECT_PROTECTED, SA_CALL_CACHE_INDICATOR, SA_CALL_TOKEN_ATTENTION) = range(6)
+ SA_CALL_SELECT_PROTECTED, SA_CALL_CACHE_INDICATOR, SA_CALL_TOKEN_ATTENTION,
+ SA_CALL_CROSS_ATTENTION) = range(7)
 
 # Every symbol the C header declares, with its ctypes signature.
 _VP, _I, _F, _SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
@@ -38,6 +39,10 @@ SIGNATURES = {
                                           _F, _VP, _I, _VP, _SZ, _VP]),
     "sa_cache_indicator": (_I, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
                                 _F, _F, _F, _F, _VP, _VP, _SZ, _VP]),
+    "sa_cross_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _I, _F, _VP,
+                                _SZ, _VP]),
+    "sa_cross_scores_from_lse": (_I, [_VP, _VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _I,
+                                      _F, _I, _VP, _VP, _VP, _I, _VP, _SZ, _VP]),
     "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "sa_last_error": (ctypes.c_char_p, []),
     "sa_version": (_I, []),
@@ -191,6 +196,46 @@ def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
         float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), ws.numel(),
         _stream()))
     return o, lse
+
+
+def sa_cross_attention(q, k, v, scale, *, o=None, lse=None, want_lse=False, ws=None):
+    """Dense cross-modal attention of q [B,H,Lq,d] over k, v [B,H,Lk,d];
+    returns (o, lse) with lse the natural-log row LSE (or None)."""
+    B, H, Lq, d = q.shape
+    Lk = k.shape[2]
+    dev = q.device
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(B, H, Lq, dtype=torch.float32, device=dev)
+    ws = _workspace(SA_CALL_CROSS_ATTENTION, B, H, Lq, Lk, d, 0, dev, ws)
+    _check(lib().sa_cross_attention(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, Lq, Lk, d, _dtype_code(q),
+        float(scale), _ptr(ws), ws.numel(), _stream()))
+    return o, lse
+
+
+def sa_cross_scores_from_lse(q_a, k_v, q_v, k_a, lse_a, lse_v, scale, block, *,
+                             sal_v_tok=None, sal_v_blk=None, sal_a_tok=None,
+                             accumulate=False, want_tok=True, ws=None):
+    """Saliency from the row LSEs of the two cross-attention forwards;
+    returns (sal_v_tok, sal_v_blk, sal_a_tok)."""
+    B, H, L_a, d = q_a.shape
+    L_v = k_v.shape[2]
+    n_b = -(-L_v // block)
+    dev = q_a.device
+    if sal_v_blk is None:
+        sal_v_blk = torch.empty(B, n_b, dtype=torch.float32, device=dev)
+    if sal_v_tok is None and want_tok:
+        sal_v_tok = torch.empty(B, L_v, dtype=torch.float32, device=dev)
+    if sal_a_tok is None and q_v is not None:
+        sal_a_tok = torch.empty(B, L_a, dtype=torch.float32, device=dev)
+    ws = _workspace(SA_CALL_CROSS_SCORES, B, H, L_v, L_a, d, block, dev, ws)
+    _check(lib().sa_cross_scores_from_lse(
+        _ptr(q_a), _ptr(k_v), _ptr(q_v), _ptr(k_a), _ptr(lse_a), _ptr(lse_v), B, H, L_v,
+        L_a, d, _dtype_code(q_a), float(scale), block, _ptr(sal_v_tok), _ptr(sal_v_blk),
+        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), ws.numel(), _stream()))
+    return sal_v_tok, sal_v_blk, sal_a_tok
 
 
 def sa_saliency_ema(sal_bar, sal, alpha):

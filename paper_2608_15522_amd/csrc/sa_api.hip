@@ -100,6 +100,13 @@ const char* sa_last_error(void) { return g_last_error.c_str(); }
 size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d, int block) {
   if (call == SA_CALL_CACHE_INDICATOR)
     return (B < 1 || L_v < 1 || L_a < 0) ? 0 : sa::cache_ws_bytes(B, L_v, L_a);
+  if (call == SA_CALL_CROSS_ATTENTION) {  // L_v carries Lq, L_a carries Lk
+    const int Lq = L_v, Lk = L_a;
+    if (B < 1 || H < 1 || Lq < 1 || Lq > sa::kMaxTokens || Lk < 1 || Lk > sa::kMaxTokens ||
+        (d != 64 && d != 128))
+      return 0;
+    return sa::token_attn_ws_bytes(B, H, Lk, d, Lq);
+  }
   if (call == SA_CALL_TOKEN_ATTENTION) {  // L_a carries k_tok
     if (B < 1 || H < 1 || L_v < 1 || L_v > sa::kMaxTokens || (d != 64 && d != 128) ||
         L_a < 0 || L_a > L_v)
@@ -158,6 +165,63 @@ int sa_cross_scores(const void* q_a, const void* k_v, const void* q_v, const voi
         static_cast<const float*>(q_a), static_cast<const float*>(k_v),
         static_cast<const float*>(q_v), static_cast<const float*>(k_a), B, H, L_v, L_a,
         d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, w, s);
+  return check_launch(fn);
+}
+
+int sa_cross_scores_from_lse(const void* q_a, const void* k_v, const void* q_v,
+                             const void* k_a, const float* lse_a, const float* lse_v, int B,
+                             int H, int L_v, int L_a, int d, int dtype, float scale, int block,
+                             float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
+                             int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sa_cross_scores_from_lse";
+  SA_TRY(check_common(fn, B, H, L_v, d, dtype, scale, block));
+  if (dtype != SA_BF16)
+    return fail(SA_ERR_UNSUPPORTED, "%s: only SA_BF16 inputs are supported", fn);
+  if (L_a < 1) return fail(SA_ERR_INVALID_ARG, "%s: L_a=%d must be >= 1", fn, L_a);
+  if (accumulate != 0 && accumulate != 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: accumulate=%d must be 0 or 1", fn, accumulate);
+  const bool rev = q_v != nullptr;
+  if ((k_a != nullptr) != rev || (sal_a_tok != nullptr) != rev || (lse_v != nullptr) != rev)
+    return fail(SA_ERR_INVALID_ARG,
+                "%s: q_v, k_a, lse_v and sal_a_tok must be all NULL or all non-NULL", fn);
+  SA_TRY(check_tensor(fn, "q_a", q_a, true, 16));
+  SA_TRY(check_tensor(fn, "k_v", k_v, true, 16));
+  SA_TRY(check_tensor(fn, "q_v", q_v, false, 16));
+  SA_TRY(check_tensor(fn, "k_a", k_a, false, 16));
+  SA_TRY(check_tensor(fn, "lse_a", lse_a, true, 4));
+  SA_TRY(check_tensor(fn, "lse_v", lse_v, false, 4));
+  SA_TRY(check_tensor(fn, "sal_v_tok", sal_v_tok, false, 4));
+  SA_TRY(check_tensor(fn, "sal_v_blk", sal_v_blk, true, 4));
+  SA_TRY(check_tensor(fn, "sal_a_tok", sal_a_tok, false, 4));
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::cross_ws_layout(B, H, L_v, L_a).total));
+  sa::launch_cross_scores_from_lse_bf16(
+      static_cast<const uint16_t*>(q_a), static_cast<const uint16_t*>(k_v),
+      static_cast<const uint16_t*>(q_v), static_cast<const uint16_t*>(k_a), lse_a, lse_v, B, H,
+      L_v, L_a, d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate,
+      static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_cross_attention(const void* q, const void* k, const void* v, void* o, float* lse,
+                       int B, int H, int Lq, int Lk, int d, int dtype, float scale, void* ws,
+                       size_t ws_bytes, void* stream) {
+  const char* fn = "sa_cross_attention";
+  SA_TRY(check_common(fn, B, H, Lk, d, dtype, scale, 128));
+  if (dtype != SA_BF16)
+    return fail(SA_ERR_UNSUPPORTED, "%s: only SA_BF16 inputs are supported", fn);
+  if (Lq < 1 || Lq > sa::kMaxTokens)
+    return fail(SA_ERR_INVALID_ARG, "%s: Lq=%d outside [1, %d]", fn, Lq, sa::kMaxTokens);
+  SA_TRY(check_tensor(fn, "q", q, true, 16));
+  SA_TRY(check_tensor(fn, "k", k, true, 16));
+  SA_TRY(check_tensor(fn, "v", v, true, 16));
+  SA_TRY(check_tensor(fn, "o", o, true, 16));
+  SA_TRY(check_tensor(fn, "lse", lse, false, 4));
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::token_attn_ws_bytes(B, H, Lk, d, Lq)));
+  sa::launch_cross_attention_bf16(static_cast<const uint16_t*>(q),
+                                  static_cast<const uint16_t*>(k),
+                                  static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o),
+                                  lse, B, H, Lq, Lk, d, scale, static_cast<char*>(ws),
+                                  static_cast<hipStream_t>(stream));
   return check_launch(fn);
 }
 

@@ -81,13 +81,15 @@ __device__ __forceinline__ float max_halves(float x) {
   return fmaxf(x, fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1])));
 }
 
-// GATHER (dense rows of protected tokens, Eq. (11) first case): workgroup row
-// j of pair (b,h) is token rows[b*n_rows + j] (rows >= n_rows, or a token
-// outside [0, L), are skipped); kv_idx, kv_cnt and order are not read.  The
-// key blocks are cut into n_split equal runs, one per workgroup: with
-// n_split == 1 the workgroup keeps every key and writes O and lse to the
-// token's own row; otherwise it writes its unnormalised O, running max m
-// (log2 units) and row sum to `part` for token_combine_kernel.
+// GATHER (dense rows): queries and outputs have Lq rows per pair, keys and
+// values L.  Workgroup row j of pair (b,h) is query rows[b*n_rows + j], or j
+// itself when rows is NULL (rows >= n_rows, or a query outside [0, Lq), are
+// skipped); kv_idx, kv_cnt and order are not read.  This serves the dense
+// rows of protected tokens (Eq. (11) first case, Lq == L) and cross-modal
+// attention (Lq != L).  The key blocks are cut into n_split equal runs, one
+// per workgroup: with n_split == 1 the workgroup keeps every key and writes
+// O and lse to the query's own row; otherwise it writes its unnormalised O,
+// running max m (log2 units) and row sum to `part` for token_combine_kernel.
 template <int D, int BLOCK, bool GATHER>
 __global__ void __launch_bounds__(BLOCK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
@@ -98,7 +100,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         const int32_t* __restrict__ kv_cnt,
                         const int32_t* __restrict__ order, int P, int L,
                         int n_b, float c, const int32_t* __restrict__ rows, int n_rows,
-                        int H, int n_split, float* __restrict__ part) {
+                        int H, int n_split, float* __restrict__ part, int Lq) {
   constexpr int NW = BLOCK / 32;             // waves per workgroup
   constexpr int TPB = BLOCK / kTile;         // tiles per key block
   constexpr int KC = D / 16;                 // k-steps of Q K^T
@@ -179,14 +181,18 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     }
   }
 
-  const uint16_t* qh = q + static_cast<size_t>(pair) * L * D;
+  const int LQ = GATHER ? Lq : L;  // query and output rows per pair
+  const uint16_t* qh = q + static_cast<size_t>(pair) * LQ * D;
   const char* kh = reinterpret_cast<const char*>(k + static_cast<size_t>(pair) * L * D);
   const char* vh = reinterpret_cast<const char*>(v + static_cast<size_t>(pair) * L * D);
 
   int qrow = r * BLOCK + (tid >> 6) * 32 + n;
   if constexpr (GATHER) {
-    qrow = qrow < n_rows ? rows[static_cast<size_t>(pair / H) * n_rows + qrow] : -1;
-    if (qrow >= L) qrow = -1;
+    if (qrow >= n_rows)
+      qrow = -1;
+    else if (rows != nullptr)
+      qrow = rows[static_cast<size_t>(pair / H) * n_rows + qrow];
+    if (qrow >= LQ) qrow = -1;
   }
   const bool qvalid = GATHER ? qrow >= 0 : qrow < L;
   u32x4 qf[KC];
@@ -342,23 +348,30 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
             32 + crow(2 * i + 1, g) < kv ? fast_exp2(fmaf(sc1[2 * i + 1], c, -m)) : 0.f;
         pb0[i] = pack_bf16x2(p0, p1);
         pb1[i] = pack_bf16x2(p2, p3);
+        if constexpr (GATHER) lsum += (p0 + p1) + (p2 + p3);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        pb0[i] = pack_bf16x2(fast_exp2(fmaf(sc0[2 * i], c, -m)),
-                             fast_exp2(fmaf(sc0[2 * i + 1], c, -m)));
-        pb1[i] = pack_bf16x2(fast_exp2(fmaf(sc1[2 * i], c, -m)),
-                             fast_exp2(fmaf(sc1[2 * i + 1], c, -m)));
+        const float p0 = fast_exp2(fmaf(sc0[2 * i], c, -m));
+        const float p1 = fast_exp2(fmaf(sc0[2 * i + 1], c, -m));
+        const float p2 = fast_exp2(fmaf(sc1[2 * i], c, -m));
+        const float p3 = fast_exp2(fmaf(sc1[2 * i + 1], c, -m));
+        pb0[i] = pack_bf16x2(p0, p1);
+        pb1[i] = pack_bf16x2(p2, p3);
+        if constexpr (GATHER) lsum += (p0 + p1) + (p2 + p3);
       }
     }
-    // row sum of the bf16 probabilities that the PV product uses
+    // row sum: of the bf16 probabilities that the PV product uses, or (GATHER)
+    // of the fp32 probabilities, so that lse is exact to fp32 rounding
+    if constexpr (!GATHER) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb0[i]), ones,
-                                             lsum, false);
-      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb1[i]), ones,
-                                             lsum, false);
+      for (int i = 0; i < 8; ++i) {
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb0[i]), ones,
+                                               lsum, false);
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb1[i]), ones,
+                                               lsum, false);
+      }
     }
     // O^T += V(t)^T P(t)^T while the row max of S(t+1) is taken.
     const lds_u16_t* Vb = (const lds_u16_t*)Vs[t & 1];
@@ -452,7 +465,10 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
         const int pk = st * PPA + u;  // 0..7 from c0, 8..15 from c1
         const f32x16& src = pk < 8 ? c0 : c1;
         const int e = 2 * (pk & 7);
-        pb[pk] = pack_bf16x2(fast_exp2(fmaf(src[e], c, -m)), fast_exp2(fmaf(src[e + 1], c, -m)));
+        const float pa = fast_exp2(fmaf(src[e], c, -m));
+        const float pc = fast_exp2(fmaf(src[e + 1], c, -m));
+        pb[pk] = pack_bf16x2(pa, pc);
+        if constexpr (GATHER) lsum += pa + pc;  // fp32 row sum (exact lse)
       }
 #pragma unroll
       for (int i = 0; i < NI; ++i)
@@ -482,8 +498,9 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       for (int u = 0; u < VB; ++u) {
         const int w = j * VB + u;  // 0..15: row sums, 16..31: max pairs
         if (w < 16) {
-          lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb[w]), ones,
-                                                 lsum, false);
+          if constexpr (!GATHER)
+            lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pb[w]), ones,
+                                                   lsum, false);
         } else {
           const int e = w - 16;  // pair e: elements 2e, 2e+1 of n0 (e < 8) or n1
           const f32x16& src = e < 8 ? n0 : n1;
@@ -547,7 +564,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   }
   const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
   if (qvalid) {
-    uint16_t* orow = o + (static_cast<size_t>(pair) * L + qrow) * D;
+    uint16_t* orow = o + (static_cast<size_t>(pair) * LQ + qrow) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
@@ -559,18 +576,19 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       }
     }
     if (lse != nullptr && g == 0)
-      lse[static_cast<size_t>(pair) * L + qrow] =
+      lse[static_cast<size_t>(pair) * LQ + qrow] =
           ltot > 0.f ? (m + __log2f(ltot)) * kLn2 : -INFINITY;
   }
 }
 
-// Merges the n_split partial rows of each protected token: with M the
-// largest running max, O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s and
+// Merges the n_split partial rows of each gathered query (rows[b*n_rows + j],
+// or j when rows is NULL; Lq output rows per pair): with M the largest
+// running max, O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s and
 // lse = (M + log2 of the denominator) ln 2, the splits added in index order.
 // One thread per 4 channels of a row.
 template <int D>
 __global__ void __launch_bounds__(256)
-token_combine_kernel(const float* __restrict__ part, int n_split, int P, int L, int H,
+token_combine_kernel(const float* __restrict__ part, int n_split, int P, int Lq, int H,
                      const int32_t* __restrict__ rows, int n_rows, uint16_t* __restrict__ o,
                      float* __restrict__ lse) {
   constexpr int TPR = D / 4;
@@ -579,8 +597,8 @@ token_combine_kernel(const float* __restrict__ part, int n_split, int P, int L, 
   if (pr >= static_cast<size_t>(P) * n_rows) return;
   const int d4 = static_cast<int>(gid % TPR) * 4;
   const int pair = static_cast<int>(pr / n_rows), j = static_cast<int>(pr % n_rows);
-  const int t = rows[static_cast<size_t>(pair / H) * n_rows + j];
-  if (t < 0 || t >= L) return;
+  const int t = rows != nullptr ? rows[static_cast<size_t>(pair / H) * n_rows + j] : j;
+  if (t < 0 || t >= Lq) return;
   const size_t stride = static_cast<size_t>(P) * n_rows;  // rows per split
   const float2* ml = reinterpret_cast<const float2*>(part + n_split * stride * D);
   float M = -INFINITY;
@@ -601,9 +619,9 @@ token_combine_kernel(const float* __restrict__ part, int n_split, int P, int L, 
   const float inv = den > 0.f ? 1.f / den : 0.f;
   const u32x2 val = {pack_bf16x2(num[0] * inv, num[1] * inv),
                      pack_bf16x2(num[2] * inv, num[3] * inv)};
-  *reinterpret_cast<u32x2*>(o + (static_cast<size_t>(pair) * L + t) * D + d4) = val;
+  *reinterpret_cast<u32x2*>(o + (static_cast<size_t>(pair) * Lq + t) * D + d4) = val;
   if (lse != nullptr && d4 == 0)
-    lse[static_cast<size_t>(pair) * L + t] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
+    lse[static_cast<size_t>(pair) * Lq + t] = den > 0.f ? (M + __log2f(den)) * kLn2 : -INFINITY;
 }
 
 // ---- fp32 path ------------------------------------------------------------
@@ -710,19 +728,19 @@ void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
   if (d == 128 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 128, false>), grid, dim3(256), 0, s,
                        q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
-                       nullptr);
+                       nullptr, L);
   else if (d == 128 && block == 64)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 64, false>), grid, dim3(128), 0, s,
                        q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
-                       nullptr);
+                       nullptr, L);
   else if (d == 64 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 128, false>), grid, dim3(256), 0, s,
                        q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
-                       nullptr);
+                       nullptr, L);
   else
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 64, false>), grid, dim3(128), 0, s,
                        q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
-                       nullptr);
+                       nullptr, L);
 }
 
 void launch_sparse_attention_f32(const float* q, const float* k,
@@ -740,38 +758,55 @@ void launch_sparse_attention_f32(const float* q, const float* k,
                        o, lse, kv_idx, kv_cnt, L, n_b, block, scale, nullptr, 0, H);
 }
 
+// Dense rows gathered from Q ([B,H,Lq,d]; rows[b*n_rows + j], or j when rows
+// is NULL) against every key of K/V ([B,H,Lk,d]), in blocks of 128 rows;
+// with more than one key split the partials go to ws and
+// token_combine_kernel writes O/lse.
+void launch_gather_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                  uint16_t* o, float* lse, int B, int H, int Lq, int Lk,
+                                  int d, float scale, const int32_t* rows, int n_rows,
+                                  char* ws, hipStream_t s) {
+  const int n_b = ceil_div(Lk, kTokRowBlock);
+  const int P = B * H;
+  const float c = scale * kLog2e;
+  const int ns = token_attn_splits(P, n_rows, n_b);
+  float* part = ns > 1 ? reinterpret_cast<float*>(ws) : nullptr;
+  const dim3 grid(P * ceil_div(n_rows, kTokRowBlock) * ns);
+  if (d == 128)
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, kTokRowBlock, true>), grid, dim3(256), 0,
+                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, Lk, n_b, c, rows,
+                       n_rows, H, ns, part, Lq);
+  else
+    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, kTokRowBlock, true>), grid, dim3(256), 0,
+                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, Lk, n_b, c, rows,
+                       n_rows, H, ns, part, Lq);
+  if (ns > 1) {
+    const size_t threads = static_cast<size_t>(P) * n_rows * (d / 4);
+    const dim3 cgrid(static_cast<unsigned>((threads + 255) / 256));
+    if (d == 128)
+      hipLaunchKernelGGL(token_combine_kernel<128>, cgrid, dim3(256), 0, s, part, ns, P, Lq, H,
+                         rows, n_rows, o, lse);
+    else
+      hipLaunchKernelGGL(token_combine_kernel<64>, cgrid, dim3(256), 0, s, part, ns, P, Lq, H,
+                         rows, n_rows, o, lse);
+  }
+}
+
 // Dense rows of the protected tokens (Eq. (11) first case), written over O
-// and lse: the gather variants, blocks of 128 gathered rows; with more than
-// one key split the partials go to ws and token_combine_kernel writes O/lse.
+// and lse.
 void launch_protected_token_attention_bf16(const uint16_t* q, const uint16_t* k,
                                            const uint16_t* v, uint16_t* o, float* lse,
                                            int B, int H, int L, int d, float scale,
                                            const int32_t* tok_idx, int k_tok, char* ws,
                                            hipStream_t s) {
-  const int n_b = ceil_div(L, kTokRowBlock);
-  const int P = B * H;
-  const float c = scale * kLog2e;
-  const int ns = token_attn_splits(P, k_tok, n_b);
-  float* part = ns > 1 ? reinterpret_cast<float*>(ws) : nullptr;
-  const dim3 grid(P * ceil_div(k_tok, kTokRowBlock) * ns);
-  if (d == 128)
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, kTokRowBlock, true>), grid, dim3(256), 0,
-                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
-                       k_tok, H, ns, part);
-  else
-    hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, kTokRowBlock, true>), grid, dim3(256), 0,
-                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, L, n_b, c, tok_idx,
-                       k_tok, H, ns, part);
-  if (ns > 1) {
-    const size_t threads = static_cast<size_t>(P) * k_tok * (d / 4);
-    const dim3 cgrid(static_cast<unsigned>((threads + 255) / 256));
-    if (d == 128)
-      hipLaunchKernelGGL(token_combine_kernel<128>, cgrid, dim3(256), 0, s, part, ns, P, L, H,
-                         tok_idx, k_tok, o, lse);
-    else
-      hipLaunchKernelGGL(token_combine_kernel<64>, cgrid, dim3(256), 0, s, part, ns, P, L, H,
-                         tok_idx, k_tok, o, lse);
-  }
+  launch_gather_attention_bf16(q, k, v, o, lse, B, H, L, L, d, scale, tok_idx, k_tok, ws, s);
+}
+
+// Cross-modal attention: every query of Q [B,H,Lq,d] against K/V [B,H,Lk,d].
+void launch_cross_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                 uint16_t* o, float* lse, int B, int H, int Lq, int Lk, int d,
+                                 float scale, char* ws, hipStream_t s) {
+  launch_gather_attention_bf16(q, k, v, o, lse, B, H, Lq, Lk, d, scale, nullptr, Lq, ws, s);
 }
 
 void launch_protected_token_attention_f32(const float* q, const float* k, const float* v,

@@ -22,6 +22,10 @@
 //                        with S and sums the column mass of each audio key.
 //   K3b v2a_chunk_sum  : fixed-order sum over video chunks per head, then
 //       v2a_finalize   : fixed-order sum over heads, / (H*L_v).
+// From the forwards: with the row LSEs of the a->v and v->a cross-attention
+// forwards (natural log, as the attention kernels write them), K1/K1b and
+// pass 1 of K3 are skipped: lse_to_log2 converts lse_a for K2, and K3 reads
+// lse_v.
 // All bf16 kernels share one key-stream engine (below).  No atomics: every
 // output element has one writer, so results are reproducible.
 // fp32 inputs use plain per-thread kernels with the same outputs.
@@ -434,11 +438,13 @@ a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
 // Q^v^T (a lane owns a video query) for its log2-sum-exp, pass 2 streams the
 // workgroup's window of 512 audio keys with S = Q^v K^a^T and sums the column
 // mass of each key over the 512 queries (per-lane LDS slots, fixed order).
-template <int D>
+// FROM_LSE: pass 1 is replaced by the natural-log LSE of each video query
+// that a v->a cross-attention forward produced (lse_v [P][L_v]).
+template <int D, bool FROM_LSE>
 __global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
                    const uint16_t* __restrict__ k_a, float* __restrict__ part,
-                   int L_v, int L_a, int nchunk, float c) {
+                   int L_v, int L_a, int nchunk, float c, const float* __restrict__ lse_v) {
   constexpr int RS = kAWin + 32;
   __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
   __shared__ float red[2 * kXW][RS];
@@ -456,8 +462,16 @@ v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
   KeyRing<D> ring;
   ring.init(ring_lds, wave, lane);
 
-  // pass 1: log2-sum-exp of every video query over all audio keys
-  {
+  if constexpr (FROM_LSE) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int row = i0 + 32 * h + n;
+      if (g == 0)
+        lse_w[wave][32 * h + n] =
+            row < L_v ? lse_v[static_cast<size_t>(pair) * L_v + row] * kLog2e : INFINITY;
+    }
+  } else {
+    // pass 1: log2-sum-exp of every video query over all audio keys
     LseAcc<D> acc;
     acc.c = c;
     acc.key_begin = 0;
@@ -642,8 +656,55 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
     float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
     float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
-    hipLaunchKernelGGL(v2a_colmass_kernel<D>, dim3(nchunk3, ceil_div(L_a, kAWin), P),
-                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c);
+    hipLaunchKernelGGL((v2a_colmass_kernel<D, false>), dim3(nchunk3, ceil_div(L_a, kAWin), P),
+                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, nullptr);
+    hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
+                       v2a_part, v2a_head, L_a, nchunk3);
+    const size_t na = static_cast<size_t>(B) * L_a;
+    hipLaunchKernelGGL(v2a_finalize_kernel, dim3((na + 255) / 256), dim3(256), 0, s,
+                       v2a_head, sal_a_tok, B, H, L_a,
+                       1.0f / (static_cast<float>(H) * static_cast<float>(L_v)), accumulate);
+  }
+}
+
+// lse2 = lse * log2(e): natural-log LSE of the scaled scores to the log2
+// units of the key-stream kernels.
+__global__ void __launch_bounds__(256)
+lse_to_log2_kernel(const float* __restrict__ lse, float* __restrict__ lse2, size_t n) {
+  for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
+       i += static_cast<size_t>(gridDim.x) * 256)
+    lse2[i] = lse[i] * kLog2e;
+}
+
+// The saliency of both directions from the row LSEs of the two cross-
+// attention forwards: K2 and K3's column-mass pass only.
+template <int D>
+void cross_bf16_from_lse(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
+                         const uint16_t* k_a, const float* lse_a, const float* lse_v, int B,
+                         int H, int L_v, int L_a, float scale, int block, float* sal_v_tok,
+                         float* sal_v_blk, float* sal_a_tok, int accumulate, char* ws,
+                         hipStream_t s) {
+  const CrossWs lay = cross_ws_layout(B, H, L_v, L_a);
+  const float c = scale * kLog2e;
+  const int P = B * H;
+  float* lse2 = reinterpret_cast<float*>(ws + lay.lse_a);
+  float* colmass = reinterpret_cast<float*>(ws + lay.colmass);
+  const size_t nlse = static_cast<size_t>(P) * L_a;
+  const size_t cblocks = (nlse + 255) / 256;
+  hipLaunchKernelGGL(lse_to_log2_kernel, dim3(static_cast<unsigned>(cblocks < 1024 ? cblocks : 1024)),
+                     dim3(256), 0, s, lse_a, lse2, nlse);
+  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColKeys), H, B), dim3(kXNT),
+                     0, s, q_a, k_v, lse2, colmass, H, L_v, L_a, c);
+  const int n_b = ceil_div(L_v, block);
+  hipLaunchKernelGGL(a2v_finalize_kernel, dim3(n_b, B), dim3(block), 0, s, colmass,
+                     sal_v_tok, sal_v_blk, L_v, H,
+                     1.0f / (static_cast<float>(H) * static_cast<float>(L_a)), accumulate);
+  if (q_v != nullptr) {
+    float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);
+    const int nchunk3 = ceil_div(L_v, kV2aChunk);
+    float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
+    hipLaunchKernelGGL((v2a_colmass_kernel<D, true>), dim3(nchunk3, ceil_div(L_a, kAWin), P),
+                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, lse_v);
     hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
                        v2a_part, v2a_head, L_a, nchunk3);
     const size_t na = static_cast<size_t>(B) * L_a;
@@ -702,6 +763,20 @@ void launch_cross_scores_bf16(const uint16_t* q_a, const uint16_t* k_v,
   else
     cross_bf16<64>(q_a, k_v, q_v, k_a, B, H, L_v, L_a, scale, block, sal_v_tok,
                    sal_v_blk, sal_a_tok, accumulate, ws, s);
+}
+
+void launch_cross_scores_from_lse_bf16(const uint16_t* q_a, const uint16_t* k_v,
+                                       const uint16_t* q_v, const uint16_t* k_a,
+                                       const float* lse_a, const float* lse_v, int B, int H,
+                                       int L_v, int L_a, int d, float scale, int block,
+                                       float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
+                                       int accumulate, char* ws, hipStream_t s) {
+  if (d == 128)
+    cross_bf16_from_lse<128>(q_a, k_v, q_v, k_a, lse_a, lse_v, B, H, L_v, L_a, scale, block,
+                             sal_v_tok, sal_v_blk, sal_a_tok, accumulate, ws, s);
+  else
+    cross_bf16_from_lse<64>(q_a, k_v, q_v, k_a, lse_a, lse_v, B, H, L_v, L_a, scale, block,
+                            sal_v_tok, sal_v_blk, sal_a_tok, accumulate, ws, s);
 }
 
 void launch_cross_scores_f32(const float* q_a, const float* k_v,

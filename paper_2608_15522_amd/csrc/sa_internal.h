@@ -136,6 +136,11 @@ void launch_protected_token_attention_bf16(const uint16_t* q, const uint16_t* k,
                                            int B, int H, int L, int d, float scale,
                                            const int32_t* tok_idx, int k_tok, char* ws,
                                            hipStream_t s);
+// Dense cross-modal attention (queries [B,H,Lq,d], keys/values [B,H,Lk,d]);
+// the workspace is token_attn_ws_bytes(B, H, Lk, d, Lq).
+void launch_cross_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                 uint16_t* o, float* lse, int B, int H, int Lq, int Lk, int d,
+                                 float scale, char* ws, hipStream_t s);
 void launch_protected_token_attention_f32(const float* q, const float* k, const float* v,
                                           float* o, float* lse, int B, int H, int L, int d,
                                           float scale, const int32_t* tok_idx, int k_tok,
@@ -146,6 +151,14 @@ void launch_cross_scores_bf16(const uint16_t* q_a, const uint16_t* k_v,
                               int block, float* sal_v_tok, float* sal_v_blk,
                               float* sal_a_tok, int accumulate, char* ws,
                               hipStream_t s);
+// Saliency from the row LSEs (natural log, [B,H,L_a] and [B,H,L_v]) of the
+// two cross-attention forwards; the workspace is cross_ws_layout's.
+void launch_cross_scores_from_lse_bf16(const uint16_t* q_a, const uint16_t* k_v,
+                                       const uint16_t* q_v, const uint16_t* k_a,
+                                       const float* lse_a, const float* lse_v, int B, int H,
+                                       int L_v, int L_a, int d, float scale, int block,
+                                       float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
+                                       int accumulate, char* ws, hipStream_t s);
 void launch_cross_scores_f32(const float* q_a, const float* k_v,
                              const float* q_v, const float* k_a, int B, int H,
                              int L_v, int L_a, int d, float scale, int block,

@@ -94,6 +94,19 @@ def test_token_attention_workspace(B, H, L, k_tok, d, splits):
     assert need == want
 
 
+def test_cross_attention_workspace():
+    """The split rule of the gathered rows with Lq rows over Lk keys."""
+    # a->v at the Ovi-like shape: 24 x 4 row blocks, 256 key blocks -> 5 runs
+    assert _splits(24, 512, 256) == 5
+    assert sa.sa_workspace_size(sa.SA_CALL_CROSS_ATTENTION, 1, 24, 512, 32760, 128, 0) == \
+        (5 * 24 * 512 * (4 * 128 + 8) + 255) // 256 * 256
+    # v->a: 6144 row blocks of 4 key blocks -> no split
+    assert sa.sa_workspace_size(sa.SA_CALL_CROSS_ATTENTION, 1, 24, 32760, 512, 128, 0) == 0
+    for bad in [(0, 1, 10, 10, 64, 0), (1, 1, 0, 10, 64, 0), (1, 1, 10, 0, 64, 0),
+                (1, 1, 10, 10, 96, 0), (1, 1, 10, 262145, 64, 0)]:
+        assert sa.sa_workspace_size(sa.SA_CALL_CROSS_ATTENTION, *bad) == 0
+
+
 def test_token_attention_workspace_rejects():
     for bad in [(0, 1, 10, 1, 64, 0), (1, 1, 10, 11, 64, 0), (1, 1, 10, -1, 64, 0),
                 (1, 1, 10, 1, 96, 0)]:
@@ -124,6 +137,22 @@ def _cross(**kw):
              ws_bytes=1 << 40, stream=None)
     a.update(kw)
     return sa.lib().sa_cross_scores(*a.values())
+
+
+def _xfwd(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, Lq=512, Lk=4000, d=128,
+             dtype=0, scale=0.088, ws=FAKE, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return sa.lib().sa_cross_attention(*a.values())
+
+
+def _xlse(**kw):
+    a = dict(q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, lse_a=FAKE, lse_v=FAKE, B=1, H=1,
+             L_v=1000, L_a=64, d=128, dtype=0, scale=0.088, block=128, sal_v_tok=None,
+             sal_v_blk=FAKE, sal_a_tok=FAKE, accumulate=0, ws=FAKE, ws_bytes=1 << 40,
+             stream=None)
+    a.update(kw)
+    return sa.lib().sa_cross_scores_from_lse(*a.values())
 
 
 def _select(**kw):
@@ -190,6 +219,20 @@ def _cache(**kw):
     (_tokens, dict(tok_idx=None), sa.SA_ERR_INVALID_ARG, "both NULL"),
     (_tokens, dict(sal_tok=None), sa.SA_ERR_INVALID_ARG, "sal_tok is NULL"),
     (_tokens, dict(tok_flag=FAKE, tok_idx=MISALIGNED + 1), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_xfwd, dict(dtype=1), sa.SA_ERR_UNSUPPORTED, "SA_BF16"),
+    (_xfwd, dict(Lq=0), sa.SA_ERR_INVALID_ARG, "Lq=0"),
+    (_xfwd, dict(Lq=262145), sa.SA_ERR_INVALID_ARG, "Lq=262145"),
+    (_xfwd, dict(Lk=2049 * 128), sa.SA_ERR_UNSUPPORTED, "n_b"),
+    (_xfwd, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
+    (_xfwd, dict(o=None), sa.SA_ERR_INVALID_ARG, "o is NULL"),
+    (_xfwd, dict(ws_bytes=4), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_xfwd, dict(scale=0.0), sa.SA_ERR_INVALID_ARG, "scale"),
+    (_xlse, dict(dtype=1), sa.SA_ERR_UNSUPPORTED, "SA_BF16"),
+    (_xlse, dict(lse_v=None), sa.SA_ERR_INVALID_ARG, "lse_v"),
+    (_xlse, dict(lse_a=None), sa.SA_ERR_INVALID_ARG, "lse_a is NULL"),
+    (_xlse, dict(q_v=None, k_a=None, sal_a_tok=None), sa.SA_ERR_INVALID_ARG, "lse_v"),
+    (_xlse, dict(L_a=0), sa.SA_ERR_INVALID_ARG, "L_a=0"),
+    (_xlse, dict(ws_bytes=4), sa.SA_ERR_WORKSPACE, "workspace"),
     (_ptok, dict(k_tok=1001), sa.SA_ERR_INVALID_ARG, "k_tok"),
     (_ptok, dict(k_tok=-1), sa.SA_ERR_INVALID_ARG, "k_tok"),
     (_ptok, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
