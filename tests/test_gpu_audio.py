@@ -24,6 +24,8 @@ CASES = [
     ("bf16_block128_La700", BASE.with_(name="a3", H=2, frames=2, rows=10, cols=13, L_a=700,
                                        n_plant=1, block_a=128, rho_a=0.1), True),
     ("f32_tiny", synth.WORKLOADS["tiny_f32"], True),
+    ("bf16_B2_La300", BASE.with_(name="a6", B=2, H=2, frames=2, rows=10, cols=13, L_a=300,
+                                 n_plant=1), True),
     # the audio shapes of the Ovi-like and LTX-like workloads; a short video
     # side, and a seeded L1-normalised map as the lagged audio saliency
     ("ovi_audio_full", BASE.with_(name="a4", frames=1, rows=1, cols=128, n_plant=0), False),

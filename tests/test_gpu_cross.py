@@ -47,6 +47,8 @@ SAL = [("small", synth.WORKLOADS["ovi_bf16"].with_(name="c1", H=2, frames=4, row
                                                    cols=13, L_a=200, n_plant=2)),
        ("d64", synth.WORKLOADS["ovi_bf16"].with_(name="c2", H=3, d=64, block=64, frames=3,
                                                  rows=10, cols=11, L_a=1000, n_plant=1)),
+       ("B2", synth.WORKLOADS["ovi_bf16"].with_(name="c3", B=2, H=2, frames=3, rows=10,
+                                                cols=13, L_a=150, n_plant=1)),
        ("ovi", synth.WORKLOADS["ovi_bf16"])]
 
 

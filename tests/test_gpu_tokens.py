@@ -90,6 +90,9 @@ LAYERS = [
     # 11 key blocks of 128: two runs of 5 and 6 blocks
     ("bf16_d64_split2", BASE.with_(name="t5", H=3, d=64, block=64, frames=2, rows=10,
                                    cols=65, L_a=40, n_plant=1), 4, 0.1),
+    # two batch items: each has its own protected tokens, shared by its heads
+    ("bf16_B2_split4", BASE.with_(name="t7", B=2, H=2, frames=4, rows=10, cols=50, L_a=64,
+                                  n_plant=2), 3, 0.05),
 ]
 
 
