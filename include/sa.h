@@ -43,7 +43,8 @@
  *   SA_ERR_HIP reports a failed kernel launch (hipGetLastError).
  * - Budgets are plain integers; the caller computes ceil(ratio * count).
  * - Supported sizes: d in {64, 128}; block in {64, 128};
- *   1 <= n_b = ceil(L_v / block) <= 2048; L_a >= 1.
+ *   1 <= n_b = ceil(L_v / block) <= 2048; L_a >= 1; B * H <= 65535 (larger
+ *   products return SA_ERR_UNSUPPORTED).
  * - Results are bit-reproducible run to run (no floating-point atomics).
  * - Scratch memory ("workspace") is passed by the caller; its minimum size is
  *   sa_workspace_size(call, ...).  A smaller ws_bytes fails with

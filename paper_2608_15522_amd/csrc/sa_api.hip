@@ -46,6 +46,9 @@ int check_common(const char* fn, int B, int H, int L, int d, int dtype, float sc
                  int block) {
   if (B < 1 || H < 1 || L < 1)
     return fail(SA_ERR_INVALID_ARG, "%s: B=%d H=%d L=%d must all be >= 1", fn, B, H, L);
+  if (static_cast<long long>(B) * H > sa::kMaxPairs)  // one grid dimension per (b, h)
+    return fail(SA_ERR_UNSUPPORTED, "%s: B*H=%lld exceeds %d", fn,
+                static_cast<long long>(B) * H, sa::kMaxPairs);
   if (dtype != SA_BF16 && dtype != SA_F32)
     return fail(SA_ERR_UNSUPPORTED, "%s: dtype %d is neither SA_BF16 nor SA_F32", fn, dtype);
   if (d != 64 && d != 128)
@@ -100,6 +103,7 @@ const char* sa_last_error(void) { return g_last_error.c_str(); }
 size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d, int block) {
   if (call == SA_CALL_CACHE_INDICATOR)
     return (B < 1 || L_v < 1 || L_a < 0) ? 0 : sa::cache_ws_bytes(B, L_v, L_a);
+  if (static_cast<long long>(B) * H > sa::kMaxPairs) return 0;
   if (call == SA_CALL_CROSS_ATTENTION) {  // L_v carries Lq, L_a carries Lk
     const int Lq = L_v, Lk = L_a;
     if (B < 1 || H < 1 || Lq < 1 || Lq > sa::kMaxTokens || Lk < 1 || Lk > sa::kMaxTokens ||

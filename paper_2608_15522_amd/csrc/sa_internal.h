@@ -14,6 +14,7 @@ constexpr int kLseChunk = 1024;   // video keys per a->v log-sum-exp partial
 constexpr int kQSlab = 512;       // queries per 16-wave workgroup slab
 constexpr int kV2aChunk = 512;    // video queries per v->a workgroup
 constexpr int kMaxBlocks = 2048;  // largest supported n_b
+constexpr int kMaxPairs = 65535;  // largest B*H (a grid dimension indexes (b, h))
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 

@@ -64,6 +64,7 @@ def test_workspace_sizes():
         assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, *bad) == 0
     assert sa.sa_workspace_size(sa.SA_CALL_CROSS_SCORES, 1, 1, 10, 0, 64, 64) == 0
     assert sa.sa_workspace_size(9, 1, 1, 10, 1, 64, 64) == 0
+    assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, 256, 256, 10, 1, 64, 64) == 0
     # cache indicator: 9 fp32 partials per workgroup (1024 video, 64 audio)
     assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 1, 0, 32760, 512, 0, 0) == \
         ((1024 + 64) * 36 + 255) // 256 * 256
@@ -247,6 +248,9 @@ def _cache(**kw):
     (_attn, dict(dtype=7), sa.SA_ERR_UNSUPPORTED, "dtype"),
     (_attn, dict(L=2049 * 128), sa.SA_ERR_UNSUPPORTED, "n_b"),
     (_attn, dict(B=0), sa.SA_ERR_INVALID_ARG, ">= 1"),
+    (_attn, dict(B=256, H=256), sa.SA_ERR_UNSUPPORTED, "B*H=65536"),
+    (_cross, dict(B=65536), sa.SA_ERR_UNSUPPORTED, "B*H=65536"),
+    (_xfwd, dict(H=70000), sa.SA_ERR_UNSUPPORTED, "B*H=70000"),
     (_attn, dict(L=0), sa.SA_ERR_INVALID_ARG, ">= 1"),
     (_attn, dict(scale=0.0), sa.SA_ERR_INVALID_ARG, "scale"),
     (_attn, dict(scale=float("nan")), sa.SA_ERR_INVALID_ARG, "scale"),
