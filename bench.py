@@ -137,7 +137,9 @@ def time_layer(plan, t, steps, warmup, torch):
              "sa_sparse_attention"]
     per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
                 for j, n in enumerate(names)}
-    return wall * 1e3 / steps, per_call
+    med = {n: sorted(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps))[steps // 2]
+           for j, n in enumerate(names)}
+    return wall * 1e3 / steps, per_call, med
 
 
 def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
@@ -427,8 +429,16 @@ def cpu_baseline(w, x, kv_idx, kv_cnt, heads):
     dt = time.perf_counter() - t0
     layer_s = dt * w.H / heads
     dense = 4.0 * w.B * w.H * w.L_v ** 2 * w.d
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in fh
+                              if ln.startswith("model name")), cpu_model)
+    except OSError:  # pragma: no cover
+        pass
     return {"value": round(dense / layer_s / 1e12, 6), "unit": "TFLOP/s",
-            "cores": int(cores), "kind": "oracle",
+            "cores": int(cores), "kind": "oracle", "cpu_model": cpu_model,
+            "numpy": np.__version__,
             "ms_per_layer": round(layer_s * 1e3, 1),
             "sample": (f"{heads} of {w.H} heads of the {w.name} layer (saliency in "
                        f"both directions, pooled-QK block mask, sparse attention on "
@@ -501,7 +511,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    ms_layer, per_call = time_layer(plan, t, args.steps, args.warmup, torch)
+    ms_layer, per_call, per_call_median = time_layer(plan, t, args.steps, args.warmup, torch)
     print(f"bench: layer {ms_layer:.3f} ms {per_call}", file=sys.stderr, flush=True)
 
     kv_idx = plan.kv_idx.cpu().numpy()
@@ -529,6 +539,7 @@ def main():
                    "d": w.d, "block": w.block, "density": w.density, "k_keep": w.k_keep,
                    "k_prot": w.k_prot, "n_b": n_b},
         "per_call_ms": {k: round(v, 4) for k, v in per_call.items()},
+        "per_call_median_ms": {k: round(v, 4) for k, v in per_call_median.items()},
         "attention": {
             "computed_tflop": round(flops_attn / 1e12, 4),
             "dense_tflop": round(dense_flops / 1e12, 4),
