@@ -3,8 +3,12 @@
 The video hot path of "Efficient Audio-Visual Generation via Synchrony-Aware
 Cross-Modal Sparse Attention" (Sec. 4.1-4.2): cross-modal saliency, protected
 block selection, the protected pooled-QK block mask and block-sparse flash
-attention, implemented as hand-written HIP kernels behind a C ABI
-(``include/sa.h``, ``libsa.so``) with a thin ctypes binding.
+attention; beside it the lagged saliency update and token-granular protection
+(Eq. (4), (8)-(11)) for either modality, the cross-modal attention forwards
+with the saliency taken from their row log-sum-exps, and the
+synchronization-aware cache-reuse indicator (Sec. 4.3).  Everything runs in
+hand-written HIP kernels behind a C ABI (``include/sa.h``, ``libsa.so``); this
+package is a thin ctypes binding over it.
 """
 from .binding import (  # noqa: F401
     SaError, lib, sa_build_block_mask, sa_cross_scores, sa_last_error,
