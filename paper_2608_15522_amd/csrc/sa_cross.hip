@@ -16,10 +16,10 @@
 //                        lane partials of a key are added in a fixed order.
 //   K2b a2v_finalize   : sum over heads, divide by H*L_a, block sums.
 // v->a: s^a_j = 1/(H*L_v) * sum_h sum_i softmax_j(scale * q^v_i . k^a_j).
-//   K3 v2a_colmass     : per (512 video queries, 512-key audio window, b*h);
-//                        pass 1 streams every audio key with S^T for each
-//                        video query's log-sum-exp, pass 2 streams the window
-//                        with S and sums the column mass of each audio key.
+//   K3 v2a_colmass     : per (512 video queries, b*h); pass 1 streams every
+//                        audio key with S^T for each video query's
+//                        log-sum-exp, pass 2 streams them again, 512 at a
+//                        time, with S and sums the column mass of each key.
 //   K3b v2a_chunk_sum  : fixed-order sum over video chunks per head, then
 //       v2a_finalize   : fixed-order sum over heads, / (H*L_v).
 // From the forwards: with the row LSEs of the a->v and v->a cross-attention
@@ -433,10 +433,10 @@ a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
 }
 
 // ---- K3 ---------------------------------------------------------------------
-// v->a column mass: grid (ceil(L_v/512), ceil(L_a/512), P).  The workgroup
-// holds 512 video queries; pass 1 streams every audio key with S^T = K^a
-// Q^v^T (a lane owns a video query) for its log2-sum-exp, pass 2 streams the
-// workgroup's window of 512 audio keys with S = Q^v K^a^T and sums the column
+// v->a column mass: grid (ceil(L_v/512), 1, P).  The workgroup holds 512
+// video queries; pass 1 streams every audio key with S^T = K^a Q^v^T (a lane
+// owns a video query) for its log2-sum-exp, pass 2 streams the audio keys
+// again, one window of 512 at a time, with S = Q^v K^a^T and sums the column
 // mass of each key over the 512 queries (per-lane LDS slots, fixed order).
 // FROM_LSE: pass 1 is replaced by the natural-log LSE of each video query
 // that a v->a cross-attention forward produced (lse_v [P][L_v]).
@@ -449,7 +449,7 @@ v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
   __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
   __shared__ float red[2 * kXW][RS];
   __shared__ float lse_w[kXW][64];
-  const int chunk = blockIdx.x, win = blockIdx.y, pair = blockIdx.z;
+  const int chunk = blockIdx.x, pair = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 5, n = lane & 31;
   const int i0 = chunk * kV2aChunk + wave * 64;  // first video query row of the wave
@@ -487,9 +487,7 @@ v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
   }
   __syncthreads();
 
-  // pass 2: column mass of the window's audio keys
-  const int key_begin = win * kAWin;
-  const int key_end = min(key_begin + kAWin, L_a);
+  // pass 2: column mass of the audio keys, one window of 512 keys at a time
   ColAcc<D> acc;
   acc.c = c;
   acc.red = &red[2 * wave + g][n];
@@ -497,14 +495,19 @@ v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
   for (int h = 0; h < 2; ++h)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc.lr[h][i] = lse_w[wave][32 * h + crow(i, g)];
-  for (int k = 0; k < kAWin; k += 32) acc.red[k] = 0.f;
-  stream_keys<D, false>(ring, ring_lds, kah, key_begin, L_a, ceil_div(key_end - key_begin, 64),
-                        qf, acc);
-  for (int k = threadIdx.x; k < key_end - key_begin; k += kXNT) {
-    float sum = 0.f;
+  for (int key_begin = 0; key_begin < L_a; key_begin += kAWin) {
+    const int key_end = min(key_begin + kAWin, L_a);
+    if (key_begin > 0) __syncthreads();  // the previous window's slots have been read
+    for (int k = 0; k < kAWin; k += 32) acc.red[k] = 0.f;
+    // ends with a barrier: every wave's slots are complete below
+    stream_keys<D, false>(ring, ring_lds, kah, key_begin, L_a,
+                          ceil_div(key_end - key_begin, 64), qf, acc);
+    for (int k = threadIdx.x; k < key_end - key_begin; k += kXNT) {
+      float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < 2 * kXW; ++w) sum += red[w][k];
-    part[(static_cast<size_t>(pair) * nchunk + chunk) * L_a + key_begin + k] = sum;
+      for (int w = 0; w < 2 * kXW; ++w) sum += red[w][k];
+      part[(static_cast<size_t>(pair) * nchunk + chunk) * L_a + key_begin + k] = sum;
+    }
   }
 }
 
@@ -656,7 +659,7 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
     float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
     float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
-    hipLaunchKernelGGL((v2a_colmass_kernel<D, false>), dim3(nchunk3, ceil_div(L_a, kAWin), P),
+    hipLaunchKernelGGL((v2a_colmass_kernel<D, false>), dim3(nchunk3, 1, P),
                        dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, nullptr);
     hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
                        v2a_part, v2a_head, L_a, nchunk3);
@@ -703,7 +706,7 @@ void cross_bf16_from_lse(const uint16_t* q_a, const uint16_t* k_v, const uint16_
     float* v2a_part = reinterpret_cast<float*>(ws + lay.v2a_part);
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
     float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
-    hipLaunchKernelGGL((v2a_colmass_kernel<D, true>), dim3(nchunk3, ceil_div(L_a, kAWin), P),
+    hipLaunchKernelGGL((v2a_colmass_kernel<D, true>), dim3(nchunk3, 1, P),
                        dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, lse_v);
     hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
                        v2a_part, v2a_head, L_a, nchunk3);
