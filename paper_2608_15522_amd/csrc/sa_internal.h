@@ -44,13 +44,17 @@ inline CrossWs cross_ws_layout(int B, int H, int L_v, int L_a) {
   return w;
 }
 
-// Column count of the pooled block means and of the mask rows: the next
-// power of two >= n_b, at least 64.
-inline int mask_n_pad(int n_b) {
-  int p = 64;
-  while (p < n_b) p <<= 1;
-  return p;
+// Column count of the pooled block means and of the mask rows: 64 * E, with
+// E the smallest of the instantiated widths {1, 2, 3, 4, 5, 6, 8, 10, 12,
+// 16, 20, 24, 32} that covers n_b (n_b <= 2048).
+inline int mask_e(int n_b) {
+  constexpr int kWidths[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32};
+  const int need = (n_b + 63) / 64;
+  for (int e : kWidths)
+    if (e >= need) return e;
+  return 32;
 }
+inline int mask_n_pad(int n_b) { return 64 * mask_e(n_b); }
 
 struct MaskWs {
   size_t qbar;   // double [B,H,d,n_pad]  pooled query means, block index innermost

@@ -150,7 +150,7 @@ constexpr int kMaskThreads = kMaskWaves * 64;
 // doubles in at most 64 KB of LDS, and from n_pad = 512 on fewer rows keep
 // phase 1 within the register budget.
 __host__ __device__ constexpr int mask_rows_per_wg(int E) {
-  return E >= 32 ? 4 : (E >= 8 ? 8 : 16);
+  return E >= 20 ? 4 : (E >= 5 ? 8 : 16);
 }
 
 // k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 distinct
@@ -201,8 +201,8 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
                   uint8_t* __restrict__ mask, float* __restrict__ scores, int P) {
   constexpr int NPAD = 64 * E;
   constexpr int R = mask_rows_per_wg(E);
-  constexpr int KP = E >= 8 ? 16 : 32;  // d-steps of key values in flight per lane
-  constexpr int CUNR = E >= 8 ? 1 : 2;   // chunk pairs unrolled (register budget)
+  constexpr int KP = E >= 5 ? 16 : 32;  // d-steps of key values in flight per lane
+  constexpr int CUNR = E >= 5 ? 1 : 2;   // chunk pairs unrolled (register budget)
   static_assert(D % (2 * KP) == 0 && R % 2 == 0, "chunking");
   __shared__ double gs[R][NPAD];
   __shared__ __attribute__((aligned(16))) double qs[D][R];
@@ -311,9 +311,16 @@ void launch_mask_build(int E, dim3 grid, hipStream_t s, const double* qbar,
   switch (E) {
     SA_MASK_CASE(1)
     SA_MASK_CASE(2)
+    SA_MASK_CASE(3)
     SA_MASK_CASE(4)
+    SA_MASK_CASE(5)
+    SA_MASK_CASE(6)
     SA_MASK_CASE(8)
+    SA_MASK_CASE(10)
+    SA_MASK_CASE(12)
     SA_MASK_CASE(16)
+    SA_MASK_CASE(20)
+    SA_MASK_CASE(24)
     SA_MASK_CASE(32)
     default: break;
   }

@@ -211,3 +211,29 @@ def test_bitwise_reproducible_and_accumulate():
                        sal_v_tok=tok2, sal_v_blk=blk2, sal_a_tok=aud2, accumulate=True)
     assert torch.equal(tok2, 2 * tok) and torch.equal(blk2, 2 * blk)
     assert torch.equal(aud2, 2 * aud)
+
+
+# the pooled means and mask rows are padded to 64 * E columns, E in
+# {1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32}: one case per width beyond
+# the powers of two, ragged tails, every list and G compared with the oracle
+@pytest.mark.parametrize("n_b,E", [(150, 3), (300, 5), (370, 6), (600, 10), (700, 12),
+                                   (1100, 20), (1400, 24)])
+def test_block_mask_at_padded_widths(n_b, E):
+    w = BASE.with_(name=f"w{n_b}", H=2, d=64, block=64, frames=1, rows=1,
+                   cols=64 * n_b - 21, L_a=16, n_plant=2)
+    assert w.n_b == n_b and -(-n_b // 64) <= E
+    k_keep = max(1, n_b // 7)
+    print(f"case mask width n_b={n_b} E={E} k_keep={k_keep}", flush=True)
+    x = synth.make_inputs(w)
+    prot = np.zeros((1, n_b), dtype=np.uint8)
+    prot[0, [0, n_b // 2, n_b - 1]] = 1
+    t = {k: to_dev(x[k], "bf16") for k in ("q_v", "k_v")}
+    kv_idx, kv_cnt, mask, scores = sa.sa_build_block_mask(
+        t["q_v"], t["k_v"], w.scale, w.block, k_keep, torch.from_numpy(prot).cuda(),
+        want_mask=True, want_scores=True)
+    torch.cuda.synchronize()
+    G = oracle.pooled_scores(x["q_v"], x["k_v"], w.scale, w.block)
+    sc = scores.cpu().numpy()
+    assert np.all(np.abs(sc - G) <= 2.0 ** -24 * np.abs(G) + 1e-12)
+    check_kv_lists(kv_idx.cpu().numpy(), kv_cnt.cpu().numpy(), prot, G, k_keep,
+                   mask.cpu().numpy())
