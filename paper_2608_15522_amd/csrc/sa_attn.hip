@@ -14,10 +14,11 @@
 // 16 keys of the same query.  P^T is packed to bf16 in registers and feeds
 // O^T += V^T P^T directly as the B operand; the V^T operand is read from the
 // key-major tile with ds_read_b64_tr_b16 (a transposing LDS read).  The row
-// sum is taken on the same bf16 probabilities with v_dot2_f32_bf16.  The
-// scale is folded into exp2; the running output is rescaled only when a
-// lane's max grows by more than 2^8.  Keys past L are -inf, rows past L are never
-// written.
+// sum is taken on the same bf16 probabilities with v_dot2_f32_bf16 (the
+// gather form adds the fp32 probabilities instead, for an lse exact to fp32
+// rounding).  The scale is folded into exp2; the running output is rescaled
+// only when a lane's max grows by more than 2^8.  Keys past L are -inf, rows
+// past L are never written.
 //
 // Query blocks of a (batch, head) pair are launched heaviest list first
 // (protected rows hold the full list).  With a pair count that is a multiple
@@ -25,6 +26,11 @@
 // so a pair's K/V blocks are shared through one XCD's L2 and only 8 pairs'
 // K/V are live in the Infinity Cache; otherwise the launch is rank-major
 // over pairs.
+//
+// Gather form: dense rows gathered by index (protected tokens) or all rows
+// of a query tensor of another length (cross-modal attention), every key
+// kept; the keys of a row block may be split into runs whose partial rows
+// token_combine_kernel merges.
 //
 // f32 path: a plain per-row online softmax with K/V tiles in LDS (used by the
 // small fp32 workloads; fp32 MFMA would not change its role).

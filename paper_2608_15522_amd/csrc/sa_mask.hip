@@ -8,7 +8,8 @@
 //    over the valid tokens of each block, accumulated in fp64 (16-byte loads,
 //    fixed-order LDS reduction; the sums of bf16/fp32 inputs are exact),
 //    stored as [d][n_pad] (block index innermost).
-// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 16 query blocks,
+// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 16, 8 or 4 query
+//    blocks (fewer for wider rows; rows padded to 64 * E columns),
 //    the pooled scores G = scale * qbar kbar^T by fp64 FMA (a few hundred
 //    MFLOP per layer; fp32 would misrank scores closer than ~1e-6, and
 //    pooled-score gaps are that small), then per row either the full list
