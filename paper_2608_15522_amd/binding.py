@@ -109,6 +109,21 @@ def _stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+def _expect(t, name, shape, dtype):
+    """The library sees only pointers: a tensor of another shape or dtype than
+    the call implies would be read or written out of bounds, so refuse it."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {dtype}")
+
+
+def _nbytes(ws):
+    return ws.numel() * ws.element_size()
+
+
 def sa_workspace_size(call: int, B: int, H: int, L_v: int, L_a: int, d: int,
                       block: int) -> int:
     return int(lib().sa_workspace_size(call, B, H, L_v, L_a, d, block))
@@ -129,6 +144,12 @@ def sa_cross_scores(q_a, k_v, q_v, k_a, scale, block, *, sal_v_tok=None,
     L_v = k_v.shape[2]
     n_b = -(-L_v // block)
     dev = q_a.device
+    _expect(k_v, "k_v", (B, H, L_v, d), q_a.dtype)
+    _expect(q_v, "q_v", (B, H, L_v, d), q_a.dtype)
+    _expect(k_a, "k_a", (B, H, L_a, d), q_a.dtype)
+    _expect(sal_v_tok, "sal_v_tok", (B, L_v), torch.float32)
+    _expect(sal_v_blk, "sal_v_blk", (B, n_b), torch.float32)
+    _expect(sal_a_tok, "sal_a_tok", (B, L_a), torch.float32)
     if sal_v_blk is None:
         sal_v_blk = torch.empty(B, n_b, dtype=torch.float32, device=dev)
     if sal_v_tok is None and want_tok:
@@ -139,7 +160,7 @@ def sa_cross_scores(q_a, k_v, q_v, k_a, scale, block, *, sal_v_tok=None,
     _check(lib().sa_cross_scores(
         _ptr(q_a), _ptr(k_v), _ptr(q_v), _ptr(k_a), B, H, L_v, L_a, d,
         _dtype_code(q_a), float(scale), block, _ptr(sal_v_tok), _ptr(sal_v_blk),
-        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), ws.numel(), _stream()))
+        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), _nbytes(ws), _stream()))
     return sal_v_tok, sal_v_blk, sal_a_tok
 
 
@@ -148,6 +169,9 @@ def sa_select_protected(sal_blk, k_prot, *, prot_idx=None, prot_flag=None,
     """Protected blocks; returns (prot_idx [B,k_prot] i32, prot_flag [B,n_b] u8)."""
     B, n_b = sal_blk.shape
     dev = sal_blk.device
+    _expect(sal_blk, "sal_blk", (B, n_b), torch.float32)
+    _expect(prot_idx, "prot_idx", (B, max(k_prot, 0)), torch.int32)
+    _expect(prot_flag, "prot_flag", (B, n_b), torch.uint8)
     if prot_idx is None and want_idx:
         prot_idx = torch.empty(B, max(k_prot, 0), dtype=torch.int32, device=dev)
     if prot_flag is None:
@@ -165,6 +189,12 @@ def sa_build_block_mask(q_v, k_v, scale, block, k_keep, prot_flag=None, *,
     B, H, L_v, d = q_v.shape
     n_b = -(-L_v // block)
     dev = q_v.device
+    _expect(k_v, "k_v", (B, H, L_v, d), q_v.dtype)
+    _expect(prot_flag, "prot_flag", (B, n_b), torch.uint8)
+    _expect(kv_idx, "kv_idx", (B, H, n_b, n_b), torch.int32)
+    _expect(kv_cnt, "kv_cnt", (B, H, n_b), torch.int32)
+    _expect(mask, "mask", (B, H, n_b, n_b), torch.uint8)
+    _expect(scores, "scores", (B, H, n_b, n_b), torch.float32)
     if kv_idx is None:
         kv_idx = torch.empty(B, H, n_b, n_b, dtype=torch.int32, device=dev)
     if kv_cnt is None:
@@ -177,7 +207,7 @@ def sa_build_block_mask(q_v, k_v, scale, block, k_keep, prot_flag=None, *,
     _check(lib().sa_build_block_mask(
         _ptr(q_v), _ptr(k_v), B, H, L_v, d, _dtype_code(q_v), float(scale), block,
         int(k_keep), _ptr(prot_flag), _ptr(kv_idx), _ptr(kv_cnt), _ptr(mask),
-        _ptr(scores), _ptr(ws), ws.numel(), _stream()))
+        _ptr(scores), _ptr(ws), _nbytes(ws), _stream()))
     return kv_idx, kv_cnt, mask, scores
 
 
@@ -186,6 +216,12 @@ def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
     """Block-sparse attention; returns (o, lse)."""
     B, H, L, d = q.shape
     dev = q.device
+    n_b = -(-L // block)
+    for name, t in (("k", k), ("v", v), ("o", o)):
+        _expect(t, name, (B, H, L, d), q.dtype)
+    _expect(lse, "lse", (B, H, L), torch.float32)
+    _expect(kv_idx, "kv_idx", (B, H, n_b, n_b), torch.int32)
+    _expect(kv_cnt, "kv_cnt", (B, H, n_b), torch.int32)
     if o is None:
         o = torch.empty_like(q)
     if lse is None and want_lse:
@@ -193,7 +229,7 @@ def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
     ws = _workspace(SA_CALL_SPARSE_ATTENTION, B, H, L, 1, d, block, dev, ws)
     _check(lib().sa_sparse_attention(
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
-        float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), ws.numel(),
+        float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), _nbytes(ws),
         _stream()))
     return o, lse
 
@@ -204,6 +240,10 @@ def sa_cross_attention(q, k, v, scale, *, o=None, lse=None, want_lse=False, ws=N
     B, H, Lq, d = q.shape
     Lk = k.shape[2]
     dev = q.device
+    _expect(k, "k", (B, H, Lk, d), q.dtype)
+    _expect(v, "v", (B, H, Lk, d), q.dtype)
+    _expect(o, "o", (B, H, Lq, d), q.dtype)
+    _expect(lse, "lse", (B, H, Lq), torch.float32)
     if o is None:
         o = torch.empty_like(q)
     if lse is None and want_lse:
@@ -211,7 +251,7 @@ def sa_cross_attention(q, k, v, scale, *, o=None, lse=None, want_lse=False, ws=N
     ws = _workspace(SA_CALL_CROSS_ATTENTION, B, H, Lq, Lk, d, 0, dev, ws)
     _check(lib().sa_cross_attention(
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, Lq, Lk, d, _dtype_code(q),
-        float(scale), _ptr(ws), ws.numel(), _stream()))
+        float(scale), _ptr(ws), _nbytes(ws), _stream()))
     return o, lse
 
 
@@ -224,6 +264,14 @@ def sa_cross_scores_from_lse(q_a, k_v, q_v, k_a, lse_a, lse_v, scale, block, *,
     L_v = k_v.shape[2]
     n_b = -(-L_v // block)
     dev = q_a.device
+    _expect(k_v, "k_v", (B, H, L_v, d), q_a.dtype)
+    _expect(q_v, "q_v", (B, H, L_v, d), q_a.dtype)
+    _expect(k_a, "k_a", (B, H, L_a, d), q_a.dtype)
+    _expect(lse_a, "lse_a", (B, H, L_a), torch.float32)
+    _expect(lse_v, "lse_v", (B, H, L_v), torch.float32)
+    _expect(sal_v_tok, "sal_v_tok", (B, L_v), torch.float32)
+    _expect(sal_v_blk, "sal_v_blk", (B, n_b), torch.float32)
+    _expect(sal_a_tok, "sal_a_tok", (B, L_a), torch.float32)
     if sal_v_blk is None:
         sal_v_blk = torch.empty(B, n_b, dtype=torch.float32, device=dev)
     if sal_v_tok is None and want_tok:
@@ -234,7 +282,7 @@ def sa_cross_scores_from_lse(q_a, k_v, q_v, k_a, lse_a, lse_v, scale, block, *,
     _check(lib().sa_cross_scores_from_lse(
         _ptr(q_a), _ptr(k_v), _ptr(q_v), _ptr(k_a), _ptr(lse_a), _ptr(lse_v), B, H, L_v,
         L_a, d, _dtype_code(q_a), float(scale), block, _ptr(sal_v_tok), _ptr(sal_v_blk),
-        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), ws.numel(), _stream()))
+        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), _nbytes(ws), _stream()))
     return sal_v_tok, sal_v_blk, sal_a_tok
 
 
@@ -254,6 +302,9 @@ def sa_select_protected_tokens(sal_tok, k_tok, *, tok_idx=None, tok_flag=None,
     """Protected tokens; returns (tok_idx [B,k_tok] i32 ascending, tok_flag [B,L] u8)."""
     B, L = sal_tok.shape
     dev = sal_tok.device
+    _expect(sal_tok, "sal_tok", (B, L), torch.float32)
+    _expect(tok_idx, "tok_idx", (B, max(k_tok, 0)), torch.int32)
+    _expect(tok_flag, "tok_flag", (B, L), torch.uint8)
     if tok_idx is None:
         tok_idx = torch.empty(B, max(k_tok, 0), dtype=torch.int32, device=dev)
     if tok_flag is None and want_flag:
@@ -268,11 +319,15 @@ def sa_protected_token_attention(q, k, v, scale, tok_idx, o, lse=None, *, ws=Non
     """Dense rows of the protected tokens written over o (and lse); returns (o, lse)."""
     B, H, L, d = q.shape
     k_tok = tok_idx.shape[1]
+    for name, t in (("k", k), ("v", v), ("o", o)):
+        _expect(t, name, (B, H, L, d), q.dtype)
+    _expect(lse, "lse", (B, H, L), torch.float32)
+    _expect(tok_idx, "tok_idx", (B, k_tok), torch.int32)
     ws = _workspace(SA_CALL_TOKEN_ATTENTION, B, H, L, k_tok, d, 0, q.device, ws)
     _check(lib().sa_protected_token_attention(
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
         float(scale), _ptr(tok_idx) if k_tok > 0 else None, int(k_tok), _ptr(ws),
-        ws.numel(), _stream()))
+        _nbytes(ws), _stream()))
     return o, lse
 
 
@@ -284,6 +339,13 @@ def sa_cache_indicator(y_v, y_v_hat, *, prot_flag=None, y_a=None, y_a_hat=None,
     B, L_v, C = y_v.shape
     L_a = y_a.shape[1] if y_a is not None else 0
     dev = y_v.device
+    _expect(y_v_hat, "y_v_hat", (B, L_v, C), y_v.dtype)
+    _expect(prot_flag, "prot_flag", (B, L_v), torch.uint8)
+    _expect(y_a, "y_a", (B, L_a, C), y_v.dtype)
+    _expect(y_a_hat, "y_a_hat", (B, L_a, C), y_v.dtype)
+    _expect(s_bar, "s_bar", (B, L_v), torch.float32)
+    _expect(s_hat, "s_hat", (B, L_v), torch.float32)
+    _expect(out, "out", (6,), torch.float32)
     if out is None:
         out = torch.empty(6, dtype=torch.float32, device=dev)
     need = sa_workspace_size(SA_CALL_CACHE_INDICATOR, B, 1, L_v, L_a, 128, 128)
@@ -292,7 +354,7 @@ def sa_cache_indicator(y_v, y_v_hat, *, prot_flag=None, y_a=None, y_a_hat=None,
     _check(lib().sa_cache_indicator(
         _ptr(y_v), _ptr(y_v_hat), _ptr(prot_flag), _ptr(y_a), _ptr(y_a_hat),
         _ptr(s_bar), _ptr(s_hat), B, L_v, L_a, C, _dtype_code(y_v), float(lambda_p),
-        float(lambda_s), float(tau), float(eps), _ptr(out), _ptr(ws), ws.numel(),
+        float(lambda_s), float(tau), float(eps), _ptr(out), _ptr(ws), _nbytes(ws),
         _stream()))
     return out
 

@@ -303,3 +303,36 @@ def test_binding_raises_without_gpu_tensors():
         sa.sa_sparse_attention(x, x, x, 0.125, 64,
                                torch.zeros(1, 1, 2, 2, dtype=torch.int32),
                                torch.zeros(1, 1, 2, dtype=torch.int32), ws=x)
+
+
+def test_binding_refuses_mismatched_tensors():
+    """The C ABI sees pointers only; the binding refuses tensors whose shape
+    or dtype disagrees with the call before anything reaches the library."""
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    q = torch.zeros(1, 2, 256, 64, dtype=bf)
+    with pytest.raises(ValueError, match="k: shape"):
+        sa.sa_sparse_attention(q, torch.zeros(1, 2, 128, 64, dtype=bf), q, 0.1, 64,
+                               torch.zeros(1, 2, 4, 4, dtype=torch.int32),
+                               torch.zeros(1, 2, 4, dtype=torch.int32))
+    with pytest.raises(TypeError, match="v: dtype"):
+        sa.sa_sparse_attention(q, q, q.float(), 0.1, 64,
+                               torch.zeros(1, 2, 4, 4, dtype=torch.int32),
+                               torch.zeros(1, 2, 4, dtype=torch.int32))
+    with pytest.raises(ValueError, match="kv_cnt: shape"):
+        sa.sa_sparse_attention(q, q, q, 0.1, 64, torch.zeros(1, 2, 4, 4, dtype=torch.int32),
+                               torch.zeros(1, 2, 3, dtype=torch.int32))
+    with pytest.raises(ValueError, match="k_v: shape"):
+        sa.sa_cross_scores(torch.zeros(1, 2, 16, 64, dtype=bf),
+                           torch.zeros(1, 3, 256, 64, dtype=bf), None, None, 0.1, 64)
+    with pytest.raises(ValueError, match="v: shape"):
+        sa.sa_cross_attention(torch.zeros(1, 2, 16, 64, dtype=bf),
+                              torch.zeros(1, 2, 100, 64, dtype=bf),
+                              torch.zeros(1, 2, 99, 64, dtype=bf), 0.1)
+    with pytest.raises(ValueError, match="tok_idx: shape"):
+        sa.sa_select_protected_tokens(torch.zeros(2, 50, dtype=f32), 5,
+                                      tok_idx=torch.zeros(2, 4, dtype=torch.int32))
+    with pytest.raises(ValueError, match="y_v_hat: shape"):
+        sa.sa_cache_indicator(torch.zeros(1, 10, 8, dtype=bf), torch.zeros(1, 9, 8, dtype=bf))
+    with pytest.raises(ValueError, match="prot_flag: shape"):
+        sa.sa_build_block_mask(q, q, 0.1, 64, 2, torch.zeros(1, 5, dtype=torch.uint8))
