@@ -16,12 +16,9 @@
 // key-major tile with ds_read_b64_tr_b16 (a transposing LDS read).  The row
 // sum is taken on the same bf16 probabilities with v_dot2_f32_bf16 (the
 // gather form adds the fp32 probabilities instead, for an lse exact to fp32
-// rounding).  Q is multiplied by scale*log2(e) and rounded to bf16 when it
-// is loaded, and the running max enters the QK^T product as its
-// accumulator's initial value, so each probability is a single exp2 (the
-// gather form keeps an fp32 FMA per logit instead, for its exact lse).  The
-// running output is rescaled only when a lane's max grows by more than 2^8.
-// Keys past L are -inf, rows past L are never written.
+// rounding).  The scale is folded into exp2; the running output is rescaled
+// only when a lane's max grows by more than 2^8.  Keys past L are -inf, rows
+// past L are never written.
 //
 // Query blocks of a (batch, head) pair are launched heaviest list first
 // (protected rows hold the full list).  With a pair count that is a multiple
@@ -118,13 +115,6 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   constexpr int NI = SPANS / NW;             // DMA instructions per wave per matrix
   constexpr int TILE_ELEMS = kTile * D;
   static_assert(SPANS % NW == 0, "tile spans must split over waves");
-  // Block-sparse form: Q is multiplied by c = scale*log2(e) and rounded to
-  // bf16 once, when it is loaded, and the running max enters S^T = K Q^T as
-  // the accumulator's initial value, so that a probability is one exp2 of
-  // the MFMA result.  The gather form keeps the fp32 product with c, so that
-  // its lse (the input of the saliency from the forwards) sees no rounding
-  // of Q beyond the input's own.
-  constexpr bool PRESCALE = !GATHER;
 
   __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][TILE_ELEMS];
   __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][TILE_ELEMS];
@@ -216,12 +206,6 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   for (int kc = 0; kc < KC; ++kc) {
     qf[kc] = qvalid ? ldg16(qh + static_cast<size_t>(qrow) * D + 16 * kc + 8 * g)
                     : u32x4{0u, 0u, 0u, 0u};
-    if constexpr (PRESCALE) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        qf[kc][e] = pack_bf16x2(__uint_as_float(qf[kc][e] << 16) * c,
-                                __uint_as_float(qf[kc][e] & 0xffff0000u) * c);
-    }
   }
 
   // DMA instruction i of wave w fills span w + NW*i of a tile: its lanes
@@ -277,63 +261,6 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 #pragma unroll
     for (int i = 0; i < NI; ++i) dma(base, off, lds, i);
   };
-  f32x16 acc[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
-  float m = -INFINITY;
-  float lsum = 0.f;
-  // PRESCALE: -m in every entry, the initial accumulator of S^T, so that S
-  // holds scaled logits relative to the running max (0 for the first tile)
-  f32x16 negm = zero16();
-  auto splat = [](float x) {
-    f32x16 r;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) r[i] = x;
-    return r;
-  };
-  // Probability of an S entry: exp2(S - m) in log2 units.
-  auto prob = [&](float sv) {
-    if constexpr (PRESCALE)
-      return fast_exp2(sv);
-    else
-      return fast_exp2(fmaf(sv, c, -m));
-  };
-  // Rescale when some lane's tile max (s0/s1, the tile whose P is formed
-  // next) exceeds the running max by more than 2^8.  PRESCALE: the tile is
-  // held relative to m and is shifted to the new max with it.
-  auto rescale = [&](float mx_lane, f32x16& s0, f32x16& s1) {
-    if constexpr (PRESCALE) {
-      const float mx = max_halves(mx_lane);
-      if (__any(mx > kRescaleSlack)) {
-        const float dm = fmaxf(mx, 0.f);
-        const float alpha = fast_exp2(-dm);
-        m += dm;
-        lsum *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          s0[i] -= dm;
-          s1[i] -= dm;
-        }
-        negm = splat(-m);
-      }
-    } else {
-      const float mx = max_halves(mx_lane) * c;
-      if (__any(mx > m + kRescaleSlack)) {
-        const float m_new = fmaxf(m, mx);
-        const float alpha = fast_exp2(m - m_new);
-        m = m_new;
-        lsum *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
-      }
-    }
-  };
   // S^T of one tile: rows 0..31 in s0, 32..63 in s1.
   // The NI copy instructions of the next K tile are spread over the k-steps
   // (one every NW/2 steps) so that no wave stalls on a full memory queue in
@@ -341,8 +268,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   auto qk = [&](auto with_copy, const uint16_t* Kt, f32x16& s0, f32x16& s1,
                 const char* dbase, const uint32_t* doff, uint16_t* dlds) {
     const char* Kb = reinterpret_cast<const char*>(Kt);
-    s0 = PRESCALE ? negm : zero16();
-    s1 = PRESCALE ? negm : zero16();
+    s0 = zero16();
+    s1 = zero16();
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       const int off = (kc & 1) ? k_off1 : k_off0;
@@ -367,6 +294,11 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     return mx;
   };
 
+  f32x16 acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
+  float m = -INFINITY;
+  float lsum = 0.f;
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
   const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
@@ -384,17 +316,6 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   if (T > 0) {
     qk(CopyFlag<false>{}, Ks[0], sc0, sc1, nullptr, nullptr, nullptr);
     mx_cur = tile_max(sc0, sc1);
-    if constexpr (PRESCALE) {
-      // the first tile sets the running max; S(0) is moved to it
-      m = max_halves(mx_cur);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        sc0[i] -= m;
-        sc1[i] -= m;
-      }
-      negm = splat(-m);
-      mx_cur = -INFINITY;
-    }
   }
   __syncthreads();  // every wave has read K(0) before iteration 0 refills its buffer
   // One iteration: the copies of K(t+2) and V(t+1) run under S(t+1) = QK^T
@@ -406,7 +327,17 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     uint32_t koff[NI], voff[NI];
     const char* kbase = prep(kh, min(t + 2, T - 1), koff);
     const char* vbase = prep(vh, min(t + 1, T - 1), voff);
-    rescale(mx_cur, sc0, sc1);
+    const float mx = max_halves(mx_cur) * c;
+    if (__any(mx > m + kRescaleSlack)) {
+      const float m_new = fmaxf(m, mx);
+      const float alpha = fast_exp2(m - m_new);
+      m = m_new;
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
+    }
     // S(t+1) on the matrix cores (computed on stale data in the last
     // iteration and discarded) while the VALUs form P(t).
     f32x16 sn0, sn1;
@@ -416,10 +347,11 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       const int kv = L - tile_key0(t);  // valid rows of this tile
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float p0 = crow(2 * i, g) < kv ? prob(sc0[2 * i]) : 0.f;
-        const float p1 = crow(2 * i + 1, g) < kv ? prob(sc0[2 * i + 1]) : 0.f;
-        const float p2 = 32 + crow(2 * i, g) < kv ? prob(sc1[2 * i]) : 0.f;
-        const float p3 = 32 + crow(2 * i + 1, g) < kv ? prob(sc1[2 * i + 1]) : 0.f;
+        const float p0 = crow(2 * i, g) < kv ? fast_exp2(fmaf(sc0[2 * i], c, -m)) : 0.f;
+        const float p1 = crow(2 * i + 1, g) < kv ? fast_exp2(fmaf(sc0[2 * i + 1], c, -m)) : 0.f;
+        const float p2 = 32 + crow(2 * i, g) < kv ? fast_exp2(fmaf(sc1[2 * i], c, -m)) : 0.f;
+        const float p3 =
+            32 + crow(2 * i + 1, g) < kv ? fast_exp2(fmaf(sc1[2 * i + 1], c, -m)) : 0.f;
         pb0[i] = pack_bf16x2(p0, p1);
         pb1[i] = pack_bf16x2(p2, p3);
         if constexpr (GATHER) lsum += (p0 + p1) + (p2 + p3);
@@ -427,10 +359,10 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     } else {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float p0 = prob(sc0[2 * i]);
-        const float p1 = prob(sc0[2 * i + 1]);
-        const float p2 = prob(sc1[2 * i]);
-        const float p3 = prob(sc1[2 * i + 1]);
+        const float p0 = fast_exp2(fmaf(sc0[2 * i], c, -m));
+        const float p1 = fast_exp2(fmaf(sc0[2 * i + 1], c, -m));
+        const float p2 = fast_exp2(fmaf(sc1[2 * i], c, -m));
+        const float p3 = fast_exp2(fmaf(sc1[2 * i + 1], c, -m));
         pb0[i] = pack_bf16x2(p0, p1);
         pb1[i] = pack_bf16x2(p2, p3);
         if constexpr (GATHER) lsum += (p0 + p1) + (p2 + p3);
@@ -486,7 +418,17 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   auto main_iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
     const char* kbase = kh + static_cast<size_t>(tile_key0(t + 2)) * D * 2;
     const char* vbase = vh + static_cast<size_t>(tile_key0(t + 1)) * D * 2;
-    rescale(mx_cur, c0, c1);
+    const float mx = max_halves(mx_cur) * c;
+    if (__any(mx > m + kRescaleSlack)) {
+      const float m_new = fmaxf(m, mx);
+      const float alpha = fast_exp2(m - m_new);
+      m = m_new;
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[dt][i] *= alpha;
+    }
     const char* Kb = reinterpret_cast<const char*>(Ks[(t + 1) & 1]);
     const lds_u16_t* Vb = (const lds_u16_t*)Vs[t & 1];
     uint16_t* kdst = Ks[t & 1];
@@ -514,8 +456,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     uint32_t pb[16];
     kread(0, ka[0]);
     kread(1, ka[1]);
-    n0 = PRESCALE ? negm : zero16();
-    n1 = PRESCALE ? negm : zero16();
+    n0 = zero16();
+    n1 = zero16();
 #pragma unroll
     for (int st = 0; st < NA; ++st) {
       const int kc = st >> 1;
@@ -529,8 +471,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
         const int pk = st * PPA + u;  // 0..7 from c0, 8..15 from c1
         const f32x16& src = pk < 8 ? c0 : c1;
         const int e = 2 * (pk & 7);
-        const float pa = prob(src[e]);
-        const float pc = prob(src[e + 1]);
+        const float pa = fast_exp2(fmaf(src[e], c, -m));
+        const float pc = fast_exp2(fmaf(src[e + 1], c, -m));
         pb[pk] = pack_bf16x2(pa, pc);
         if constexpr (GATHER) lsum += pa + pc;  // fp32 row sum (exact lse)
       }

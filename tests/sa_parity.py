@@ -13,16 +13,8 @@ import paper_2608_15522_amd as sa
 
 TIE = 1e-6          # scores within this of the k-th value may go either way
 TOL_O = {"f32": 1e-5, "bf16": 1.5e-2}
-# lse of the gather form (dense rows, cross-modal forwards): fp32 logits and
-# an fp32 row sum of fp32 probabilities; bf16 budget 2.5e-3.
-TOL_LSE_GATHER = {"f32": 1e-5, "bf16": 2.5e-3}
-# lse of the block-sparse kernel.  Its row sum adds the bf16-rounded
-# probabilities (each <= 2^-8 relative, averaging out along the row), and its
-# logits come from Q*c rounded to bf16 once (c = scale*log2 e): a logit moves
-# by scale * sum_d q_d k_d eps_d with |eps_d| <= 2^-8, about 2.6e-3 rms for
-# unit-variance inputs at d = 128 and up to ~1.2e-2 over a million pairs.
-# The lse moves by at most its row's largest shift, hence 2e-2.
-TOL_LSE = {"f32": 1e-5, "bf16": 2e-2}
+TOL_LSE = {"f32": 1e-5, "bf16": 2.5e-3}   # bf16: the row sum adds the bf16-rounded
+                                             # probabilities (<= 2^-9 relative each)
 TOL_SAL = 1e-6      # on L1-normalised saliency (diagnostic bound)
 
 

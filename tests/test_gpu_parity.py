@@ -153,6 +153,60 @@ def test_dense_lists_match_dense_attention(dtype, d, block):
     assert np.abs(lse.cpu().numpy() - lse_ref).max() <= TOL_LSE[dtype]
 
 
+def _logit_ramp_inputs(L, d, H, profile, dtype, seed=7):
+    """Q/K whose logits follow a profile along the keys: q_i = 0.5 z + 2 sqrt(d) u,
+    k_j = 0.5 z' + b_j sqrt(d) u with u a unit vector, so that scale * q_i . k_j
+    is about 2 sqrt(d) b_j (b_j up to 3: logits up to ~68, ~98 in log2 units)."""
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    j = np.arange(L) / L
+    b = {"grow": 3.0 * j, "fall": 3.0 * (1.0 - j),
+         "jump": np.where(np.arange(L) >= L - 50, 4.5, 0.0)}[profile]
+    q = 0.5 * rng.standard_normal((1, H, L, d)) + 2.0 * np.sqrt(d) * u
+    k = 0.5 * rng.standard_normal((1, H, L, d)) + (b * np.sqrt(d))[None, None, :, None] * u
+    v = rng.standard_normal((1, H, L, d))
+    out = [a.astype(np.float32) for a in (q, k, v)]
+    if dtype == "bf16":
+        out = [synth.round_to_bf16(a).reshape(a.shape) for a in out]
+    return out
+
+
+@pytest.mark.parametrize("profile", ["grow", "fall", "jump"])
+@pytest.mark.parametrize("dtype,d,block", [("bf16", 128, 128), ("bf16", 64, 64),
+                                           ("f32", 64, 64)])
+def test_running_max_under_large_logit_changes(profile, dtype, d, block):
+    """Logits that rise by ~98 log2 units along the keys (the running max is
+    raised many times, in the steady-state loop and in the tail tiles), fall
+    by as much (later tiles underflow), or jump by ~146 log2 units in the last
+    50 keys (exp2 would overflow fp32 without raising the max first), against
+    dense fp64 attention."""
+    L, H = 2000, 2
+    scale = float(np.float32(1.0 / np.sqrt(d)))
+    q, k, v = _logit_ramp_inputs(L, d, H, profile, dtype)
+    print(f"case ramp {profile} {dtype} d={d} block={block} L={L}", flush=True)
+    n_b = -(-L // block)
+    kv_idx = np.tile(np.arange(n_b, dtype=np.int32), (1, H, n_b, 1))
+    kv_cnt = np.full((1, H, n_b), n_b, dtype=np.int32)
+    o, lse = sa.sa_sparse_attention(to_dev(q, dtype), to_dev(k, dtype), to_dev(v, dtype),
+                                    scale, block, torch.from_numpy(kv_idx).cuda(),
+                                    torch.from_numpy(kv_cnt).cuda(), want_lse=True)
+    O_ref, lse_ref = oracle.dense_attention(q, k, v, scale)
+    o = o.float().cpu().numpy()
+    assert np.all(np.isfinite(o))
+    o_err = float(np.abs(o - O_ref).max())
+    l_err = float(np.abs(lse.cpu().numpy() - lse_ref).max())
+    # fp32 logits carry a rounding error in proportion to their size (~110
+    # here against ~1 in the unit-variance workloads), so the fp32 bounds
+    # scale with the largest |logit| / 10; the bf16 bounds (set by the bf16
+    # probabilities) hold as they are.
+    big = max(float(np.abs(q[0, h].astype(np.float64) @ k[0, h].T.astype(np.float64)).max())
+              for h in range(H)) * scale
+    grow = 1.0 if dtype == "bf16" else max(1.0, big / 10.0)
+    print(profile, dtype, dict(o_err=o_err, lse_err=l_err, max_logit=big), flush=True)
+    assert o_err <= TOL_O[dtype] * grow and l_err <= TOL_LSE[dtype] * grow
+
+
 def test_protected_rows_equal_the_dense_run_bitwise():
     """Eq. (11): a protected query block walks every key block in ascending
     order, exactly as the dense run of the same kernel does."""
