@@ -9,6 +9,7 @@ import numpy as np
 import torch
 
 import oracle
+import synth
 import paper_2608_15522_amd as sa
 
 TIE = 1e-6          # scores within this of the k-th value may go either way
@@ -26,6 +27,28 @@ def to_dev(x, dtype):
     t = torch.from_numpy(np.ascontiguousarray(x))
     t = t.to(torch.bfloat16 if dtype == "bf16" else torch.float32)
     return t.to("cuda")
+
+
+def logit_ramp_inputs(Lq, Lk, d, H, profile, dtype, seed=7):
+    """Q [1,H,Lq,d] and K, V [1,H,Lk,d] whose logits follow a profile along
+    the keys: q_i = 0.5 z + 2 sqrt(d) u, k_j = 0.5 z' + b_j sqrt(d) u with u a
+    unit vector, so that scale * q_i . k_j is about 2 sqrt(d) b_j.  "grow":
+    b_j rises from 0 to 3 (logits up to ~70, ~100 log2 units), "fall": the
+    reverse, "jump": b_j = 4.5 on the last 50 keys and 0 before (a jump of
+    ~150 log2 units, past fp32's exp2 range)."""
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    j = np.arange(Lk) / Lk
+    b = {"grow": 3.0 * j, "fall": 3.0 * (1.0 - j),
+         "jump": np.where(np.arange(Lk) >= Lk - 50, 4.5, 0.0)}[profile]
+    q = 0.5 * rng.standard_normal((1, H, Lq, d)) + 2.0 * np.sqrt(d) * u
+    k = 0.5 * rng.standard_normal((1, H, Lk, d)) + (b * np.sqrt(d))[None, None, :, None] * u
+    v = rng.standard_normal((1, H, Lk, d))
+    out = [a.astype(np.float32) for a in (q, k, v)]
+    if dtype == "bf16":
+        out = [synth.round_to_bf16(a).reshape(a.shape) for a in out]
+    return out
 
 
 def check_topk_set(chosen, scores, k, tie=TIE):

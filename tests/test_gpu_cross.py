@@ -8,7 +8,7 @@ import torch
 import oracle
 import synth
 import paper_2608_15522_amd as sa
-from sa_parity import TOL_LSE, TOL_O, TOL_SAL, to_dev, workers
+from sa_parity import TOL_LSE, TOL_O, TOL_SAL, logit_ramp_inputs, to_dev, workers
 
 pytestmark = pytest.mark.gpu
 
@@ -40,6 +40,29 @@ def test_cross_attention_matches_oracle(B, H, Lq, Lk, d):
     o_err = float(np.abs(_np(o) - O_ref).max())
     l_err = float(np.abs(_np(lse) - lse_ref).max())
     print(dict(o_err=o_err, lse_err=l_err), flush=True)
+    assert o_err <= TOL_O["bf16"] and l_err <= TOL_LSE["bf16"]
+
+
+@pytest.mark.parametrize("profile", ["grow", "jump"])
+@pytest.mark.parametrize("Lq,Lk", [(64, 4000), (300, 1000)])
+def test_cross_attention_under_large_logit_changes(profile, Lq, Lk):
+    """Logits rising by ~100 log2 units along the keys, or jumping by ~150 in
+    the last 50: the running max of each key run, and the merge of runs whose
+    maxima differ by that much (Lq = 64: the keys of a row block are cut into
+    runs), against dense fp64 attention."""
+    d, H = 128, 2
+    ws = sa.sa_workspace_size(sa.SA_CALL_CROSS_ATTENTION, 1, H, Lq, Lk, d, 0)
+    print(f"case cross ramp {profile} Lq={Lq} Lk={Lk} ws={ws}", flush=True)
+    q, k, v = logit_ramp_inputs(Lq, Lk, d, H, profile, "bf16")
+    scale = float(np.float32(1.0 / np.sqrt(d)))
+    o, lse = sa.sa_cross_attention(to_dev(q, "bf16"), to_dev(k, "bf16"), to_dev(v, "bf16"),
+                                   scale, want_lse=True)
+    torch.cuda.synchronize()
+    O_ref, lse_ref = oracle.dense_attention(q, k, v, scale)
+    o_err = float(np.abs(_np(o) - O_ref).max())
+    l_err = float(np.abs(_np(lse) - lse_ref).max())
+    print(profile, dict(o_err=o_err, lse_err=l_err), flush=True)
+    assert np.all(np.isfinite(_np(o)))
     assert o_err <= TOL_O["bf16"] and l_err <= TOL_LSE["bf16"]
 
 

@@ -9,7 +9,7 @@ import oracle
 import synth
 import paper_2608_15522_amd as sa
 from sa_parity import (TOL_LSE, TOL_O, check_kv_lists, compare_layer, gpu_layer,
-                       to_dev)
+                       logit_ramp_inputs, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -153,25 +153,6 @@ def test_dense_lists_match_dense_attention(dtype, d, block):
     assert np.abs(lse.cpu().numpy() - lse_ref).max() <= TOL_LSE[dtype]
 
 
-def _logit_ramp_inputs(L, d, H, profile, dtype, seed=7):
-    """Q/K whose logits follow a profile along the keys: q_i = 0.5 z + 2 sqrt(d) u,
-    k_j = 0.5 z' + b_j sqrt(d) u with u a unit vector, so that scale * q_i . k_j
-    is about 2 sqrt(d) b_j (b_j up to 3: logits up to ~68, ~98 in log2 units)."""
-    rng = np.random.default_rng(seed)
-    u = rng.standard_normal(d)
-    u /= np.linalg.norm(u)
-    j = np.arange(L) / L
-    b = {"grow": 3.0 * j, "fall": 3.0 * (1.0 - j),
-         "jump": np.where(np.arange(L) >= L - 50, 4.5, 0.0)}[profile]
-    q = 0.5 * rng.standard_normal((1, H, L, d)) + 2.0 * np.sqrt(d) * u
-    k = 0.5 * rng.standard_normal((1, H, L, d)) + (b * np.sqrt(d))[None, None, :, None] * u
-    v = rng.standard_normal((1, H, L, d))
-    out = [a.astype(np.float32) for a in (q, k, v)]
-    if dtype == "bf16":
-        out = [synth.round_to_bf16(a).reshape(a.shape) for a in out]
-    return out
-
-
 @pytest.mark.parametrize("profile", ["grow", "fall", "jump"])
 @pytest.mark.parametrize("dtype,d,block", [("bf16", 128, 128), ("bf16", 64, 64),
                                            ("f32", 64, 64)])
@@ -183,7 +164,7 @@ def test_running_max_under_large_logit_changes(profile, dtype, d, block):
     dense fp64 attention."""
     L, H = 2000, 2
     scale = float(np.float32(1.0 / np.sqrt(d)))
-    q, k, v = _logit_ramp_inputs(L, d, H, profile, dtype)
+    q, k, v = logit_ramp_inputs(L, L, d, H, profile, dtype)
     print(f"case ramp {profile} {dtype} d={d} block={block} L={L}", flush=True)
     n_b = -(-L // block)
     kv_idx = np.tile(np.arange(n_b, dtype=np.int32), (1, H, n_b, 1))
