@@ -8,8 +8,8 @@
 //    over the valid tokens of each block, accumulated in fp64 (16-byte loads,
 //    fixed-order LDS reduction; the sums of bf16/fp32 inputs are exact),
 //    stored as [d][n_pad] (block index innermost).
-// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 16, 8 or 4 query
-//    blocks (fewer for wider rows; rows padded to 64 * E columns),
+// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 8 or 4 query
+//    blocks (4 for the widest rows; rows padded to 64 * E columns),
 //    the pooled scores G = scale * qbar kbar^T by fp64 FMA (a few hundred
 //    MFLOP per layer; fp32 would misrank scores closer than ~1e-6, and
 //    pooled-score gaps are that small), then per row either the full list
@@ -148,10 +148,12 @@ constexpr int kMaskWaves = 4;
 constexpr int kMaskThreads = kMaskWaves * 64;
 
 // Query-block rows per mask workgroup: the row exchange holds rows x n_pad
-// doubles in at most 64 KB of LDS, and from n_pad = 512 on fewer rows keep
-// phase 1 within the register budget.
+// doubles in at most 64 KB of LDS, and from n_pad = 1280 on fewer rows keep
+// phase 1 within the register budget.  Below that, 8 rows rather than 16
+// give twice the workgroups and hide more of the key-mean loads (10 % less
+// time at n_b = 256).
 __host__ __device__ constexpr int mask_rows_per_wg(int E) {
-  return E >= 20 ? 4 : (E >= 5 ? 8 : 16);
+  return E >= 20 ? 4 : 8;
 }
 
 // k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 distinct
