@@ -182,10 +182,13 @@ int sa_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
  *
  * The sparse pattern S_m is pooled-QK block top-k: Q and K are averaged over
  * each block of `block` tokens (the last block over its true length), the
- * pooled score is G[r,c] = scale * qbar_r . kbar_c in fp32, and every query
- * block r that is not protected keeps the k_keep key blocks of largest
- * G[r,:] (equal scores: lower block index first).  A protected query block
- * keeps every key block; protection adds rows only.
+ * pooled score is G[r,c] = scale * qbar_r . kbar_c, means and products in
+ * fp64, and every query block r that is not protected keeps the k_keep key
+ * blocks of largest G[r,:].  Equal scores go to the lower block index first;
+ * the ranking compares the fp64 scores with their lowest 12 mantissa bits
+ * dropped, so two scores within about 2^-40 relative of each other count as
+ * equal.  A protected query block keeps every key block; protection adds
+ * rows only.
  *
  *   q_v, k_v   [B,H,L_v,d] video queries and keys
  *   k_keep     1 <= k_keep <= n_b
@@ -195,7 +198,8 @@ int sa_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
  *              ascending order, first kv_cnt entries valid, the rest -1
  *   kv_cnt     [B,H,n_b] i32 out
  *   mask       [B,H,n_b,n_b] u8 out (1 = kept), nullable
- *   scores     [B,H,n_b,n_b] f32 out: the pooled scores G, nullable
+ *   scores     [B,H,n_b,n_b] f32 out: the fp64 pooled scores G rounded once
+ *              to fp32, nullable
  *   ws         workspace of at least sa_workspace_size(SA_CALL_BUILD_BLOCK_MASK)
  */
 int sa_build_block_mask(const void* q_v, const void* k_v, int B, int H,
@@ -338,6 +342,14 @@ const char* sa_last_error(void);
 
 /* Library ABI version (major * 100 + minor). */
 int sa_version(void);
+
+/*
+ * Identity of the sources the library was built from: the first 16 hex
+ * digits of a sha256 over the kernel sources, the internal headers and this
+ * header ("unknown" for a build that did not supply it).  A caller that has
+ * the sources can compare it before use; the Python binding does.
+ */
+const char* sa_build_id(void);
 
 #ifdef __cplusplus
 }

@@ -15,6 +15,8 @@ from typing import Optional
 
 import torch
 
+from .srcid import source_id
+
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsa.so")
 
 SA_OK, SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED, SA_ERR_WORKSPACE, SA_ERR_HIP = range(5)
@@ -46,6 +48,7 @@ SIGNATURES = {
     "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "sa_last_error": (ctypes.c_char_p, []),
     "sa_version": (_I, []),
+    "sa_build_id": (ctypes.c_char_p, []),
 }
 
 
@@ -70,6 +73,12 @@ def lib():
             fn = getattr(handle, name)
             fn.restype = res
             fn.argtypes = args
+        built = handle.sa_build_id().decode()
+        want = source_id()
+        if want is not None and built != want:
+            raise SaError(-1, f"{LIB_PATH} was built from other sources (build id "
+                              f"{built}, sources {want}): rebuild it with "
+                              "`python -m paper_2608_15522_amd.build`")
         _lib_handle = handle
     return _lib_handle
 
@@ -80,6 +89,10 @@ def sa_last_error() -> str:
 
 def sa_version() -> int:
     return lib().sa_version()
+
+
+def sa_build_id() -> str:
+    return lib().sa_build_id().decode()
 
 
 def _check(rc: int):

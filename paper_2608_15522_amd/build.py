@@ -11,6 +11,12 @@ import os
 import subprocess
 import sys
 
+try:
+    from .srcid import source_id
+except ImportError:  # run as a script
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from paper_2608_15522_amd.srcid import source_id
+
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
@@ -30,9 +36,9 @@ CFLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
+def _compile(src: str, defines=()) -> str:
     obj = os.path.join(OBJ, os.path.basename(src).replace(".hip", ".o"))
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CFLAGS, *defines, "-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{res.stderr}")
@@ -54,8 +60,10 @@ def build(verbose: bool = False) -> str:
     os.makedirs(OBJ, exist_ok=True)
     srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
                   if f.endswith(".hip"))
+    # the library reports the sources it was built from (sa_build_id)
+    defines = [f'-DSA_SRC_ID="{source_id()}"']
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs) + 1)) as ex:
-        objs = list(ex.map(_compile, srcs + [BENCH_SRC]))
+        objs = list(ex.map(lambda f: _compile(f, defines), srcs + [BENCH_SRC]))
     _link(objs[:-1], LIB)
     _link(objs[-1:], BENCH_LIB)
     if verbose:

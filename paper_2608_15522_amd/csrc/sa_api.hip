@@ -86,6 +86,10 @@ int check_ws(const char* fn, const void* ws, size_t ws_bytes, size_t need) {
   return SA_OK;
 }
 
+#ifndef SA_SRC_ID
+#define SA_SRC_ID "unknown"
+#endif
+
 #define SA_TRY(expr)          \
   do {                        \
     const int rc_ = (expr);   \
@@ -97,6 +101,8 @@ int check_ws(const char* fn, const void* ws, size_t ws_bytes, size_t need) {
 extern "C" {
 
 int sa_version(void) { return 100; }
+
+const char* sa_build_id(void) { return SA_SRC_ID; }
 
 const char* sa_last_error(void) { return g_last_error.c_str(); }
 

@@ -36,6 +36,13 @@ def test_exports_every_declared_symbol():
     assert sa.sa_version() == 100
 
 
+def test_library_matches_the_sources():
+    """The binding refuses a library built from other sources; the one that
+    loaded reports the id of the sources in the tree."""
+    from paper_2608_15522_amd.srcid import source_id
+    assert sa.sa_build_id() == source_id()
+
+
 @pytest.mark.skipif(not os.path.exists(binding.BENCH_LIB_PATH),
                     reason="libsa_bench.so not built")
 def test_bench_library_exports_and_rejects_bad_arguments():
