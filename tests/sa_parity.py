@@ -16,7 +16,11 @@ TIE = 1e-6          # scores within this of the k-th value may go either way
 TOL_O = {"f32": 1e-5, "bf16": 1.5e-2}
 TOL_LSE = {"f32": 1e-5, "bf16": 2.5e-3}   # bf16: the row sum adds the bf16-rounded
                                              # probabilities (<= 2^-9 relative each)
-TOL_SAL = 1e-6      # on L1-normalised saliency (diagnostic bound)
+TOL_SAL = 1e-6      # absolute, on L1-normalised saliency (the survey's diagnostic bound)
+# Saliency is also bounded relative to each value: a token's saliency is about
+# 1/L (3e-5 at L = 32760), so the absolute bound alone would allow a few
+# percent.  fp32 exponentials and sums give ~1e-6 relative.
+SAL_REL, SAL_ABS = 1e-4, 1e-9
 
 
 def workers():
@@ -71,6 +75,38 @@ def check_topk_set(chosen, scores, k, tie=TIE):
     return int(np.sum(np.abs(scores - vk) <= tie)) - 1
 
 
+def check_saliency(got, ref, name="saliency"):
+    """|got - ref| <= SAL_REL |ref| + SAL_ABS elementwise, and <= TOL_SAL.
+    Returns the largest relative error."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    err = np.abs(got - ref)
+    bad = err > SAL_REL * np.abs(ref) + SAL_ABS
+    assert not bad.any(), (name, int(bad.sum()), float(err[bad].max()),
+                           float(np.abs(ref[bad]).min()))
+    assert float(err.max()) <= TOL_SAL, (name, float(err.max()))
+    return float((err / np.maximum(np.abs(ref), 1e-30)).max())
+
+
+def check_token_selection(tok_idx, sal_ref, k):
+    """Protected tokens against the oracle's fp64 saliency: per batch item an
+    ascending list of k tokens forming a top-k, where tokens whose reference
+    saliency lies within the relative saliency bound (twice, for both sides)
+    of the k-th value may go either way.  Returns the number of such
+    tokens."""
+    tok_idx = np.asarray(tok_idx)
+    ties = 0
+    for b in range(sal_ref.shape[0]):
+        lst = tok_idx[b]
+        assert np.all(np.diff(lst) > 0)
+        if k == 0:
+            continue
+        vk = float(sal_ref[b][oracle.topk_order(sal_ref[b], k)[-1]])
+        ties += check_topk_set(lst, sal_ref[b], k, tie=2 * (SAL_REL * abs(vk) + SAL_ABS))
+    return ties
+
+
 def check_rank_order(prot_idx, scores, tie=TIE):
     """Rank order of a top-k list: scores descending; among scores equal
     within the tie window any order is accepted."""
@@ -116,6 +152,45 @@ def check_kv_lists(kv_idx, kv_cnt, prot_flag, G_ref, k_keep, mask=None):
     return ties
 
 
+def full_masked_attention(q, k, v, scale, block, kv_idx, kv_cnt):
+    """oracle.masked_attention over every query block, its (b, h) slabs run
+    concurrently in threads (the oracle is called unchanged, once per slab)."""
+    from concurrent.futures import ThreadPoolExecutor
+    B, H, N, d = q.shape
+    n_b = -(-N // block)
+    O = np.zeros((B, H, N, v.shape[3]), dtype=np.float64)
+    lse = np.full((B, H, N), -np.inf, dtype=np.float64)
+
+    def run(bh):
+        b, h = bh
+        rows = [(b, h, r) for r in range(n_b)]
+        o_d, l_d = oracle.masked_attention(q, k, v, scale, block, kv_idx, kv_cnt, rows=rows)
+        for (_, _, r) in rows:
+            lo, hi = r * block, min((r + 1) * block, N)
+            O[b, h, lo:hi] = o_d[(b, h, r)]
+            lse[b, h, lo:hi] = l_d[(b, h, r)]
+
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1), ThreadPoolExecutor(max_workers=workers()) as ex:
+        list(ex.map(run, [(b, h) for b in range(B) for h in range(H)]))
+    return O, lse
+
+
+def sample_rows(g, w, n_random=16, seed=0):
+    """Query blocks whose attention is compared at full size: every protected
+    block of head 0, the first block and the ragged last block of each batch
+    item, and random ones."""
+    rng = np.random.default_rng(seed)
+    rows = {(0, 0, int(r)) for r in np.nonzero(g["prot_flag"][0])[0]}
+    for b in range(w.B):
+        rows.add((b, w.H - 1, w.n_b - 1))
+        rows.add((b, 0, 0))
+    for _ in range(n_random):
+        rows.add((int(rng.integers(w.B)), int(rng.integers(w.H)),
+                  int(rng.integers(w.n_b))))
+    return sorted(rows)
+
+
 def gpu_layer(x, w, k_keep, k_prot, with_audio=True):
     """All four C-ABI calls on the workload's inputs, with every optional
     output requested.  Returns numpy copies."""
@@ -153,11 +228,11 @@ def compare_layer(x, w, g, k_keep, k_prot, rows=None, with_audio=True,
     s_blk = oracle.token_to_block_saliency(s_v, w.block)
     rep["sal_v_tok_err"] = float(np.abs(g["sal_v_tok"] - s_v).max())
     rep["sal_v_blk_err"] = float(np.abs(g["sal_v_blk"] - s_blk).max())
-    assert rep["sal_v_tok_err"] <= TOL_SAL, rep
-    assert rep["sal_v_blk_err"] <= TOL_SAL, rep
+    rep["sal_v_tok_rel"] = check_saliency(g["sal_v_tok"], s_v, "sal_v_tok")
+    rep["sal_v_blk_rel"] = check_saliency(g["sal_v_blk"], s_blk, "sal_v_blk")
     if with_audio:
         rep["sal_a_tok_err"] = float(np.abs(g["sal_a_tok"] - s_a).max())
-        assert rep["sal_a_tok_err"] <= TOL_SAL, rep
+        rep["sal_a_tok_rel"] = check_saliency(g["sal_a_tok"], s_a, "sal_a_tok")
     rep["prot_ties"] = check_protected(g["prot_idx"], g["prot_flag"], s_blk, k_prot)
     G = oracle.pooled_scores(x["q_v"], x["k_v"], w.scale, w.block)
     # the scores output is the fp64 score rounded once to fp32
@@ -165,9 +240,13 @@ def compare_layer(x, w, g, k_keep, k_prot, rows=None, with_audio=True,
     assert np.all(np.abs(g["scores"] - G) <= 2.0 ** -24 * np.abs(G) + 1e-12), rep
     rep["mask_ties"] = check_kv_lists(g["kv_idx"], g["kv_cnt"], g["prot_flag"],
                                       G, k_keep, g["mask"])
-    O_ref, lse_ref = oracle.masked_attention(x["q_v"], x["k_v"], x["v_v"],
-                                             w.scale, w.block, g["kv_idx"],
-                                             g["kv_cnt"], rows=rows)
+    if rows is None:
+        O_ref, lse_ref = full_masked_attention(x["q_v"], x["k_v"], x["v_v"], w.scale,
+                                               w.block, g["kv_idx"], g["kv_cnt"])
+    else:
+        O_ref, lse_ref = oracle.masked_attention(x["q_v"], x["k_v"], x["v_v"],
+                                                 w.scale, w.block, g["kv_idx"],
+                                                 g["kv_cnt"], rows=rows)
     if rows is None:
         o_err = np.abs(g["o"] - O_ref).max()
         l_err = np.abs(g["lse"] - lse_ref).max()

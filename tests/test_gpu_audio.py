@@ -10,7 +10,8 @@ import torch
 import oracle
 import synth
 import paper_2608_15522_amd as sa
-from sa_parity import (TOL_LSE, TOL_O, TOL_SAL, check_kv_lists, to_dev, workers)
+from sa_parity import (TOL_LSE, TOL_O, check_kv_lists, check_saliency,
+                       check_token_selection, to_dev, workers)
 
 pytestmark = pytest.mark.gpu
 
@@ -73,7 +74,10 @@ def test_audio_branch_matches_oracle(name, w, from_cross):
     if from_cross:
         _, s_a = oracle.cross_scores(x["q_a"], x["k_v"], w.scale, x["q_v"], x["k_a"],
                                      workers=workers())
-        assert float(np.abs(g["sal_a"] - s_a).max()) <= TOL_SAL
+        check_saliency(g["sal_a"], s_a, "sal_a_tok")
+        # the protected audio tokens against the oracle's fp64 saliency
+        check_token_selection(g["tok_idx"], s_a, w.k_tok_a)
+    # and bit-exact against the oracle's selection on the same fp32 values
     ref_idx, ref_flag = oracle.select_protected_tokens(g["sal_a"], w.k_tok_a)
     assert np.array_equal(g["tok_idx"], ref_idx)
     assert np.array_equal(g["tok_flag"], ref_flag)

@@ -36,6 +36,12 @@ SMALL = [
     ("f32_d128_b128",
      synth.WORKLOADS["tiny_f32"].with_(name="g", d=128, block=128, frames=5, rows=10,
                                        cols=20, L_a=70, n_plant=2), 2, 1),
+    # B*H a multiple of 8: the attention launch places whole heads on XCDs
+    # (the branch the full-size layers take); d 128, block 128, ragged tails
+    ("bf16_d128_b128_BH8_tail10",
+     BASE.with_(name="i", H=8, frames=5, rows=10, cols=77, L_a=96, n_plant=3), 7, 3),
+    ("bf16_d128_b128_BH16_tail56",
+     BASE.with_(name="j", B=2, H=8, frames=3, rows=12, cols=62, L_a=64, n_plant=2), 5, 2),
 ]
 
 

@@ -9,7 +9,8 @@ import torch
 import oracle
 import synth
 import paper_2608_15522_amd as sa
-from sa_parity import TOL_LSE, TOL_O, to_dev
+from sa_parity import (TOL_LSE, TOL_O, check_saliency, check_token_selection, to_dev,
+                       workers)
 
 pytestmark = pytest.mark.gpu
 
@@ -130,6 +131,11 @@ def test_token_protected_layer_matches_oracle(name, w, k_keep, rho):
           f"k_keep={k_keep} k_tok={k_tok}", flush=True)
     x = synth.make_inputs(w)
     g = gpu_token_layer(x, w, k_keep, k_tok)
+    # the saliency and the protected tokens against the oracle's fp64 saliency
+    s_v, _ = oracle.cross_scores(x["q_a"], x["k_v"], w.scale, workers=workers())
+    check_saliency(g["sal_v_tok"], s_v, "sal_v_tok")
+    check_token_selection(g["tok_idx"], s_v, k_tok)
+    # and bit-exact against the oracle's selection on the same fp32 values
     ref_idx, ref_flag = oracle.select_protected_tokens(g["sal_v_tok"], k_tok)
     assert np.array_equal(g["tok_idx"], ref_idx)
     assert np.array_equal(g["tok_flag"], ref_flag)
@@ -152,6 +158,11 @@ def test_token_protected_layer_fullsize_ovi():
     x = synth.make_inputs(w)
     g = gpu_token_layer(x, w, w.k_keep, k_tok)
     print("ovi tokens: gpu done", flush=True)
+    s_v, _ = oracle.cross_scores(x["q_a"], x["k_v"], w.scale, workers=workers())
+    rel = check_saliency(g["sal_v_tok"], s_v, "sal_v_tok")
+    ties = check_token_selection(g["tok_idx"], s_v, k_tok)
+    print(f"ovi tokens: saliency rel err {rel:.2e}, {ties} tokens in the tie window",
+          flush=True)
     ref_idx, _ = oracle.select_protected_tokens(g["sal_v_tok"], k_tok)
     assert np.array_equal(g["tok_idx"], ref_idx)
     check_untouched(g)
