@@ -96,6 +96,37 @@ int check_ws(const char* fn, const void* ws, size_t ws_bytes, size_t need) {
     if (rc_ != SA_OK) return rc_; \
   } while (0)
 
+int check_sparse_attention_args(const char* fn, const void* q, const void* k, const void* v,
+                                const void* o, const float* lse, int B, int H, int L, int d,
+                                int dtype, float scale, int block, const int32_t* kv_idx,
+                                const int32_t* kv_cnt) {
+  SA_TRY(check_common(fn, B, H, L, d, dtype, scale, block));
+  SA_TRY(check_tensor(fn, "q", q, true, 16));
+  SA_TRY(check_tensor(fn, "k", k, true, 16));
+  SA_TRY(check_tensor(fn, "v", v, true, 16));
+  SA_TRY(check_tensor(fn, "o", o, true, 16));
+  SA_TRY(check_tensor(fn, "lse", lse, false, 4));
+  SA_TRY(check_tensor(fn, "kv_idx", kv_idx, true, 4));
+  SA_TRY(check_tensor(fn, "kv_cnt", kv_cnt, true, 4));
+  return SA_OK;
+}
+
+void launch_sparse_attention(const void* q, const void* k, const void* v, void* o, float* lse,
+                             int B, int H, int L, int d, int dtype, float scale, int block,
+                             const int32_t* kv_idx, const int32_t* kv_cnt, char* ws,
+                             hipStream_t s) {
+  if (dtype == SA_BF16)
+    sa::launch_sparse_attention_bf16(
+        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+        static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, B, H, L, d,
+        scale, block, kv_idx, kv_cnt, ws, s);
+  else
+    sa::launch_sparse_attention_f32(
+        static_cast<const float*>(q), static_cast<const float*>(k),
+        static_cast<const float*>(v), static_cast<float*>(o), lse, B, H, L, d, scale,
+        block, kv_idx, kv_cnt, ws, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -125,8 +156,9 @@ size_t sa_workspace_size(int call, int B, int H, int L_v, int L_a, int d, int bl
   }
   if (B < 1 || H < 1 || L_v < 1 || (d != 64 && d != 128) || (block != 64 && block != 128))
     return 0;
+  // in 64 bits: L_v + block - 1 overflows int for L_v near INT_MAX
+  if ((static_cast<long long>(L_v) + block - 1) / block > sa::kMaxBlocks) return 0;
   const int n_b = sa::ceil_div(L_v, block);
-  if (n_b > sa::kMaxBlocks) return 0;
   switch (call) {
     case SA_CALL_CROSS_SCORES:
       if (L_a < 1) return 0;
@@ -281,27 +313,12 @@ int sa_sparse_attention(const void* q, const void* k, const void* v, void* o, fl
                         const int32_t* kv_idx, const int32_t* kv_cnt, void* ws,
                         size_t ws_bytes, void* stream) {
   const char* fn = "sa_sparse_attention";
-  SA_TRY(check_common(fn, B, H, L, d, dtype, scale, block));
-  SA_TRY(check_tensor(fn, "q", q, true, 16));
-  SA_TRY(check_tensor(fn, "k", k, true, 16));
-  SA_TRY(check_tensor(fn, "v", v, true, 16));
-  SA_TRY(check_tensor(fn, "o", o, true, 16));
-  SA_TRY(check_tensor(fn, "lse", lse, false, 4));
-  SA_TRY(check_tensor(fn, "kv_idx", kv_idx, true, 4));
-  SA_TRY(check_tensor(fn, "kv_cnt", kv_cnt, true, 4));
+  SA_TRY(check_sparse_attention_args(fn, q, k, v, o, lse, B, H, L, d, dtype, scale, block,
+                                     kv_idx, kv_cnt));
   const int n_b = sa::ceil_div(L, block);
   SA_TRY(check_ws(fn, ws, ws_bytes, sa::attn_ws_layout(B, H, n_b, d, block).total));
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dtype == SA_BF16)
-    sa::launch_sparse_attention_bf16(
-        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-        static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), lse, B, H, L, d,
-        scale, block, kv_idx, kv_cnt, static_cast<char*>(ws), s);
-  else
-    sa::launch_sparse_attention_f32(
-        static_cast<const float*>(q), static_cast<const float*>(k),
-        static_cast<const float*>(v), static_cast<float*>(o), lse, B, H, L, d, scale,
-        block, kv_idx, kv_cnt, static_cast<char*>(ws), s);
+  launch_sparse_attention(q, k, v, o, lse, B, H, L, d, dtype, scale, block, kv_idx, kv_cnt,
+                          static_cast<char*>(ws), static_cast<hipStream_t>(stream));
   return check_launch(fn);
 }
 

@@ -190,13 +190,6 @@ cache_finish_kernel(const float* __restrict__ part, int nwg, int has_prot, int h
 
 }  // namespace
 
-int cache_workgroups_video(size_t rows_v) {
-  return static_cast<int>(rows_v < 1024 ? rows_v : 1024);  // one round on 256 CUs
-}
-int cache_workgroups_audio(size_t rows_a) {
-  return static_cast<int>(rows_a < 64 ? rows_a : 64);
-}
-
 void launch_cache_indicator(const void* y_v, const void* y_v_hat, const uint8_t* prot_flag,
                             const void* y_a, const void* y_a_hat, const float* s_bar,
                             const float* s_hat, int B, int L_v, int L_a, int C, int dtype,

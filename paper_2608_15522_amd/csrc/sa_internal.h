@@ -88,9 +88,13 @@ inline AttnWs attn_ws_layout(int B, int H, int n_b, int /*d*/, int /*block*/) {
 // ---- launchers (defined in the kernel sources) ----------------------------
 constexpr int kMaxTokens = kMaxBlocks * 128;  // longest token sequence (L)
 // Cache-reuse indicator: 9 fp32 partial sums per workgroup of the first pass
-// ([9][workgroups]).
-int cache_workgroups_video(size_t rows_v);
-int cache_workgroups_audio(size_t rows_a);
+// ([9][workgroups]); 1024 video workgroups fill one round of 256 CUs x 4.
+inline int cache_workgroups_video(size_t rows_v) {
+  return static_cast<int>(rows_v < 1024 ? rows_v : 1024);
+}
+inline int cache_workgroups_audio(size_t rows_a) {
+  return static_cast<int>(rows_a < 64 ? rows_a : 64);
+}
 inline size_t cache_ws_bytes(int B, int L_v, int L_a) {
   const size_t nwg = static_cast<size_t>(cache_workgroups_video(static_cast<size_t>(B) * L_v)) +
                      cache_workgroups_audio(static_cast<size_t>(B) * (L_a > 0 ? L_a : 0));

@@ -79,6 +79,22 @@ def test_workspace_sizes():
     assert sa.sa_workspace_size(sa.SA_CALL_CACHE_INDICATOR, 0, 0, 10, 0, 0, 0) == 0
 
 
+class _Call:
+    """One C entry point with default arguments (keyword order = C order);
+    calling it with overrides passes them positionally through ctypes."""
+
+    def __init__(self, name, **defaults):
+        self.name, self.defaults = name, defaults
+
+    def args(self, **kw):
+        a = dict(self.defaults)
+        a.update(kw)
+        return list(a.values())
+
+    def __call__(self, **kw):
+        return getattr(sa.lib(), self.name)(*self.args(**kw))
+
+
 def _splits(P, k_tok, n_b):
     """The key-split rule of the protected-token rows, restated."""
     units = P * -(-k_tok // 128)
@@ -122,85 +138,55 @@ def test_token_attention_workspace_rejects():
     assert sa.sa_workspace_size(sa.SA_CALL_TOKEN_ATTENTION, 1, 24, 32760, 0, 128, 0) == 0
 
 
-def _attn(**kw):
-    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
+_attn = _Call("sa_sparse_attention", q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
              dtype=0, scale=0.088, block=128, kv_idx=FAKE, kv_cnt=FAKE, ws=FAKE,
              ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return sa.lib().sa_sparse_attention(*a.values())
 
 
-def _mask(**kw):
-    a = dict(q_v=FAKE, k_v=FAKE, B=1, H=1, L_v=1000, d=128, dtype=0, scale=0.088,
+_mask = _Call("sa_build_block_mask", q_v=FAKE, k_v=FAKE, B=1, H=1, L_v=1000, d=128, dtype=0, scale=0.088,
              block=128, k_keep=2, prot_flag=None, kv_idx=FAKE, kv_cnt=FAKE,
              mask=None, scores=None, ws=FAKE, ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return sa.lib().sa_build_block_mask(*a.values())
 
 
-def _cross(**kw):
-    a = dict(q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, B=1, H=1, L_v=1000, L_a=64,
+_cross = _Call("sa_cross_scores", q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, B=1, H=1, L_v=1000, L_a=64,
              d=128, dtype=0, scale=0.088, block=128, sal_v_tok=None,
              sal_v_blk=FAKE, sal_a_tok=FAKE, accumulate=0, ws=FAKE,
              ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return sa.lib().sa_cross_scores(*a.values())
 
 
-def _xfwd(**kw):
-    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, Lq=512, Lk=4000, d=128,
+_xfwd = _Call("sa_cross_attention", q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, Lq=512, Lk=4000, d=128,
              dtype=0, scale=0.088, ws=FAKE, ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return sa.lib().sa_cross_attention(*a.values())
 
 
-def _xlse(**kw):
-    a = dict(q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, lse_a=FAKE, lse_v=FAKE, B=1, H=1,
+_xlse = _Call("sa_cross_scores_from_lse", q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, lse_a=FAKE, lse_v=FAKE, B=1, H=1,
              L_v=1000, L_a=64, d=128, dtype=0, scale=0.088, block=128, sal_v_tok=None,
              sal_v_blk=FAKE, sal_a_tok=FAKE, accumulate=0, ws=FAKE, ws_bytes=1 << 40,
              stream=None)
-    a.update(kw)
-    return sa.lib().sa_cross_scores_from_lse(*a.values())
 
 
-def _select(**kw):
-    a = dict(sal_blk=FAKE, B=1, n_b=8, k_prot=2, prot_idx=None, prot_flag=FAKE,
+_select = _Call("sa_select_protected", sal_blk=FAKE, B=1, n_b=8, k_prot=2, prot_idx=None, prot_flag=FAKE,
              stream=None)
-    a.update(kw)
-    return sa.lib().sa_select_protected(*a.values())
 
 
-def _ema(**kw):
-    a = dict(sal_bar=FAKE, sal=FAKE, n=1000, alpha=0.5, stream=None)
-    a.update(kw)
-    return sa.lib().sa_saliency_ema(*a.values())
+_ema = _Call("sa_saliency_ema", sal_bar=FAKE, sal=FAKE, n=1000, alpha=0.5, stream=None)
 
 
-def _tokens(**kw):
-    a = dict(sal_tok=FAKE, B=1, L=1000, k_tok=50, tok_idx=FAKE, tok_flag=None,
+_tokens = _Call("sa_select_protected_tokens", sal_tok=FAKE, B=1, L=1000, k_tok=50, tok_idx=FAKE, tok_flag=None,
              stream=None)
-    a.update(kw)
-    return sa.lib().sa_select_protected_tokens(*a.values())
 
 
-def _ptok(**kw):
-    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
+_ptok = _Call("sa_protected_token_attention", q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
              dtype=0, scale=0.088, tok_idx=FAKE, k_tok=10, ws=FAKE, ws_bytes=1 << 40,
              stream=None)
-    a.update(kw)
-    return sa.lib().sa_protected_token_attention(*a.values())
 
 
-def _cache(**kw):
-    a = dict(y_v=FAKE, y_v_hat=FAKE, prot_flag=None, y_a=None, y_a_hat=None,
+_cache = _Call("sa_cache_indicator", y_v=FAKE, y_v_hat=FAKE, prot_flag=None, y_a=None, y_a_hat=None,
              s_bar=None, s_hat=None, B=1, L_v=1000, L_a=0, C=64, dtype=0,
              lambda_p=0.5, lambda_s=0.1, tau=0.2, eps=1e-6, out=FAKE, ws=FAKE,
              ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return sa.lib().sa_cache_indicator(*a.values())
 
 
-@pytest.mark.parametrize("call,kw,code,needle", [
+INVALID = [
     (_cache, dict(C=12), sa.SA_ERR_INVALID_ARG, "multiple of 8"),
     (_cache, dict(C=0), sa.SA_ERR_INVALID_ARG, "multiple of 8"),
     (_cache, dict(B=1 << 20, L_v=1 << 10, C=1 << 16), sa.SA_ERR_INVALID_ARG, "too large"),
@@ -289,7 +275,10 @@ def _cache(**kw):
     (_select, dict(n_b=4096, k_prot=1), sa.SA_ERR_UNSUPPORTED, "n_b"),
     (_select, dict(prot_flag=None), sa.SA_ERR_INVALID_ARG, "prot_flag is NULL"),
     (_select, dict(sal_blk=MISALIGNED + 1), sa.SA_ERR_INVALID_ARG, "aligned"),
-])
+]
+
+
+@pytest.mark.parametrize("call,kw,code,needle", INVALID)
 def test_invalid_arguments_are_rejected(call, kw, code, needle):
     rc = call(**kw)
     assert rc == code
