@@ -232,6 +232,31 @@ int sa_sparse_attention(const void* q, const void* k, const void* v, void* o,
                         void* stream);
 
 /*
+ * sa_sparse_attention_noalloc -- sa_sparse_attention without a workspace
+ * argument and without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid hipMalloc).
+ *
+ * Arguments, results and errors are those of sa_sparse_attention; the same
+ * kernels run, so the outputs are bitwise those of sa_sparse_attention.  The
+ * scratch (the per-head launch order of the query blocks, B*H*n_b int32) lives
+ * in a 4 MiB array that the library holds on each device it runs on until the
+ * process ends, so B*H*n_b <= 1048576; larger sizes fail with
+ * SA_ERR_UNSUPPORTED before any launch.  Every element of the scratch that a
+ * call reads is written by that call first, so nothing has to be cleared.
+ * All calls on one device share the array: calls that overlap in time on one
+ * device (on different streams, or from different threads) race and must be
+ * serialised by the caller.  `stream` must belong to the current device.
+ * The first call on a device looks up the array's device address
+ * (hipGetSymbolAddress), which needs no allocation.
+ */
+int sa_sparse_attention_noalloc(const void* q, const void* k, const void* v,
+                                void* o, float* lse, int B, int H, int L,
+                                int d, int dtype, float scale, int block,
+                                const int32_t* kv_idx, const int32_t* kv_cnt,
+                                void* stream);
+
+/*
  * sa_saliency_ema -- one update of the lagged saliency cache (Sec. 4.1,
  * Eq. (4)): sal_bar[i] = alpha * sal_bar[i] + (1 - alpha) * sal[i] for
  * i < n, in fp32.  The refresh schedule (every K denoising steps) is the

@@ -12,7 +12,7 @@ package is a thin ctypes binding over it.
 """
 from .binding import (  # noqa: F401
     SaError, lib, sa_build_block_mask, sa_cross_scores, sa_last_error,
-    sa_select_protected, sa_sparse_attention, sa_version, sa_build_id, sa_workspace_size,
+    sa_select_protected, sa_sparse_attention, sa_sparse_attention_noalloc, sa_version, sa_build_id, sa_workspace_size,
     sa_saliency_ema, sa_select_protected_tokens, sa_protected_token_attention,
     sa_cache_indicator, SA_CALL_CACHE_INDICATOR, SA_CALL_TOKEN_ATTENTION,
     sa_cross_attention, sa_cross_scores_from_lse, SA_CALL_CROSS_ATTENTION,

@@ -35,6 +35,8 @@ SIGNATURES = {
                                  _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "sa_sparse_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _F,
                                  _I, _VP, _VP, _VP, _SZ, _VP]),
+    "sa_sparse_attention_noalloc": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _F,
+                                         _I, _VP, _VP, _VP]),
     "sa_saliency_ema": (_I, [_VP, _VP, _SZ, _F, _VP]),
     "sa_select_protected_tokens": (_I, [_VP, _I, _I, _I, _VP, _VP, _VP]),
     "sa_protected_token_attention": (_I, [_VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I,
@@ -244,6 +246,22 @@ def sa_sparse_attention(q, k, v, scale, block, kv_idx, kv_cnt, *, o=None,
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
         float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _ptr(ws), _nbytes(ws),
         _stream()))
+    return o, lse
+
+
+def sa_sparse_attention_noalloc(q, k, v, scale, block, kv_idx, kv_cnt, o, lse=None):
+    """Block-sparse attention into the caller's o (and lse), with the
+    library's own per-device scratch: nothing is allocated.  Returns (o, lse)."""
+    B, H, L, d = q.shape
+    n_b = -(-L // block)
+    for name, t in (("k", k), ("v", v), ("o", o)):
+        _expect(t, name, (B, H, L, d), q.dtype)
+    _expect(lse, "lse", (B, H, L), torch.float32)
+    _expect(kv_idx, "kv_idx", (B, H, n_b, n_b), torch.int32)
+    _expect(kv_cnt, "kv_cnt", (B, H, n_b), torch.int32)
+    _check(lib().sa_sparse_attention_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, L, d, _dtype_code(q),
+        float(scale), block, _ptr(kv_idx), _ptr(kv_cnt), _stream()))
     return o, lse
 
 

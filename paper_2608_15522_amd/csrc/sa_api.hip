@@ -5,13 +5,23 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/sa.h"
 #include "sa_device.h"
 #include "sa_internal.h"
 
+// Scratch of sa_sparse_attention_noalloc: each device holds its own copy of
+// this array until the process ends.  Calls on one device share it.
+constexpr size_t kStaticScratchBytes = static_cast<size_t>(4) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
 namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+char* g_scratch_ptr[kMaxScratchDevices];  // device address of scratch, per device
 
 thread_local std::string g_last_error;
 
@@ -125,6 +135,40 @@ void launch_sparse_attention(const void* q, const void* k, const void* v, void* 
         static_cast<const float*>(q), static_cast<const float*>(k),
         static_cast<const float*>(v), static_cast<float*>(o), lse, B, H, L, d, scale,
         block, kv_idx, kv_cnt, ws, s);
+}
+
+// The device address of `scratch` on the device that runs stream s, looked up
+// on the first call on that device (with it current) and kept.  The array's
+// host-side name is not a device address; only the address returned here is
+// passed to kernels.
+int static_scratch(const char* fn, hipStream_t s, char** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess)
+    return fail(SA_ERR_HIP, "%s: hipGetDevice failed: %s", fn, hipGetErrorString(e));
+  if (s != nullptr) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(s, &sdev);
+    if (e != hipSuccess)
+      return fail(SA_ERR_HIP, "%s: hipStreamGetDevice failed: %s", fn, hipGetErrorString(e));
+    if (sdev != dev)
+      return fail(SA_ERR_INVALID_ARG, "%s: the stream belongs to device %d, not to the "
+                  "current device %d", fn, static_cast<int>(sdev), dev);
+  }
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(SA_ERR_UNSUPPORTED, "%s: device %d outside [0, %d)", fn, dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SA_ERR_HIP, "%s: hipGetSymbolAddress(scratch) failed on device %d: %s", fn,
+                  dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return SA_OK;
 }
 
 }  // namespace
@@ -319,6 +363,29 @@ int sa_sparse_attention(const void* q, const void* k, const void* v, void* o, fl
   SA_TRY(check_ws(fn, ws, ws_bytes, sa::attn_ws_layout(B, H, n_b, d, block).total));
   launch_sparse_attention(q, k, v, o, lse, B, H, L, d, dtype, scale, block, kv_idx, kv_cnt,
                           static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_sparse_attention_noalloc(const void* q, const void* k, const void* v, void* o,
+                                float* lse, int B, int H, int L, int d, int dtype, float scale,
+                                int block, const int32_t* kv_idx, const int32_t* kv_cnt,
+                                void* stream) {
+  const char* fn = "sa_sparse_attention_noalloc";
+  SA_TRY(check_sparse_attention_args(fn, q, k, v, o, lse, B, H, L, d, dtype, scale, block,
+                                     kv_idx, kv_cnt));
+  const int n_b = sa::ceil_div(L, block);
+  const size_t need = sa::attn_ws_layout(B, H, n_b, d, block).total;
+  if (need > kStaticScratchBytes)
+    return fail(SA_ERR_UNSUPPORTED,
+                "%s: B=%d H=%d n_b=%d needs %zu bytes of scratch, above the %zu bytes the "
+                "library holds per device (B*H*n_b <= %zu); call sa_sparse_attention with a "
+                "workspace instead", fn, B, H, n_b, need, kStaticScratchBytes,
+                kStaticScratchBytes / sizeof(int32_t));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = nullptr;
+  SA_TRY(static_scratch(fn, s, &ws));
+  launch_sparse_attention(q, k, v, o, lse, B, H, L, d, dtype, scale, block, kv_idx, kv_cnt,
+                          ws, s);
   return check_launch(fn);
 }
 

@@ -55,6 +55,12 @@ bool dispatch(const std::string& name, size_t a, int* rc) {
                               I(a + 6), I(a + 7), I(a + 8), I(a + 9), F(a + 10), I(a + 11),
                               Pt<const int32_t>(a + 12), Pt<const int32_t>(a + 13), P(a + 14),
                               Z(a + 15), P(a + 16));
+  } else if (name == "sa_sparse_attention_noalloc") {
+    need(15);
+    *rc = sa_sparse_attention_noalloc(P(a), P(a + 1), P(a + 2), P(a + 3), Pt<float>(a + 4),
+                                      I(a + 5), I(a + 6), I(a + 7), I(a + 8), I(a + 9),
+                                      F(a + 10), I(a + 11), Pt<const int32_t>(a + 12),
+                                      Pt<const int32_t>(a + 13), P(a + 14));
   } else if (name == "sa_build_block_mask") {
     need(18);
     *rc = sa_build_block_mask(P(a), P(a + 1), I(a + 2), I(a + 3), I(a + 4), I(a + 5), I(a + 6),

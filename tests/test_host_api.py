@@ -143,6 +143,10 @@ _attn = _Call("sa_sparse_attention", q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B
              ws_bytes=1 << 40, stream=None)
 
 
+_attn_na = _Call("sa_sparse_attention_noalloc", q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, H=1, L=1000, d=128,
+             dtype=0, scale=0.088, block=128, kv_idx=FAKE, kv_cnt=FAKE, stream=None)
+
+
 _mask = _Call("sa_build_block_mask", q_v=FAKE, k_v=FAKE, B=1, H=1, L_v=1000, d=128, dtype=0, scale=0.088,
              block=128, k_keep=2, prot_flag=None, kv_idx=FAKE, kv_cnt=FAKE,
              mask=None, scores=None, ws=FAKE, ws_bytes=1 << 40, stream=None)
@@ -255,6 +259,11 @@ INVALID = [
     (_attn, dict(lse=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
     (_attn, dict(ws_bytes=16), sa.SA_ERR_WORKSPACE, "workspace"),
     (_attn, dict(ws=None), sa.SA_ERR_INVALID_ARG, "ws is NULL"),
+    (_attn_na, dict(q=None), sa.SA_ERR_INVALID_ARG, "q is NULL"),
+    (_attn_na, dict(kv_cnt=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_attn_na, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
+    # B*H*n_b = 600 * 2048 entries of launch order exceed the 4 MiB scratch
+    (_attn_na, dict(H=600, L=262144), sa.SA_ERR_UNSUPPORTED, "scratch"),
     (_mask, dict(k_keep=0), sa.SA_ERR_INVALID_ARG, "k_keep"),
     (_mask, dict(k_keep=9), sa.SA_ERR_INVALID_ARG, "k_keep"),
     (_mask, dict(kv_idx=None), sa.SA_ERR_INVALID_ARG, "kv_idx is NULL"),

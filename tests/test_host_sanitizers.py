@@ -12,7 +12,7 @@ import subprocess
 import pytest
 
 import paper_2608_15522_amd as sa
-from test_host_api import FAKE, INVALID, _attn, _mask, _select
+from test_host_api import INVALID, _attn, _mask, _select
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HERE = os.path.join(ROOT, "tests", "host_asan")
