@@ -239,11 +239,13 @@ int sa_sparse_attention(const void* q, const void* k, const void* v, void* o,
  *
  * Arguments, results and errors are those of sa_sparse_attention; the same
  * kernels run, so the outputs are bitwise those of sa_sparse_attention.  The
- * scratch (the per-head launch order of the query blocks, B*H*n_b int32) lives
- * in a 4 MiB array that the library holds on each device it runs on until the
- * process ends, so B*H*n_b <= 1048576; larger sizes fail with
+ * scratch (the launch order and schedule of the query blocks, two arrays of
+ * B*H*n_b int32, and 8 row counters) lives in a 4 MiB array that the library
+ * holds on each device it runs on until the process ends, so
+ * B*H*n_b <= 524032; larger sizes fail with
  * SA_ERR_UNSUPPORTED before any launch.  Every element of the scratch that a
- * call reads is written by that call first, so nothing has to be cleared.
+ * call reads is written by that call first (the row counters are set to zero
+ * by a kernel of the same call), so nothing has to be cleared beforehand.
  * All calls on one device share the array: calls that overlap in time on one
  * device (on different streams, or from different threads) race and must be
  * serialised by the caller.  `stream` must belong to the current device.

@@ -378,9 +378,8 @@ int sa_sparse_attention_noalloc(const void* q, const void* k, const void* v, voi
   if (need > kStaticScratchBytes)
     return fail(SA_ERR_UNSUPPORTED,
                 "%s: B=%d H=%d n_b=%d needs %zu bytes of scratch, above the %zu bytes the "
-                "library holds per device (B*H*n_b <= %zu); call sa_sparse_attention with a "
-                "workspace instead", fn, B, H, n_b, need, kStaticScratchBytes,
-                kStaticScratchBytes / sizeof(int32_t));
+                "library holds per device; call sa_sparse_attention with a workspace "
+                "instead", fn, B, H, n_b, need, kStaticScratchBytes);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = nullptr;
   SA_TRY(static_scratch(fn, s, &ws));

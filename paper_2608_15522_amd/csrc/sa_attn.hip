@@ -22,10 +22,10 @@
 //
 // Query blocks of a (batch, head) pair are launched heaviest list first
 // (protected rows hold the full list).  With a pair count that is a multiple
-// of 8, each XCD takes every 8th pair and works through them one at a time,
-// so a pair's K/V blocks are shared through one XCD's L2 and only 8 pairs'
-// K/V are live in the Infinity Cache; otherwise the launch is rank-major
-// over pairs.
+// of 8, each XCD takes every 8th pair: first the full rows of all its pairs,
+// then the other rows one pair at a time, so that a pair's K/V blocks are
+// shared through one XCD's L2 and the long full rows do not run alone at the
+// end of the launch; otherwise the launch is rank-major over pairs.
 //
 // Gather form: dense rows gathered by index (protected tokens) or all rows
 // of a query tensor of another length (cross-modal attention), every key
@@ -34,13 +34,16 @@
 //
 // f32 path: a plain per-row online softmax with K/V tiles in LDS (used by the
 // small fp32 workloads; fp32 MFMA would not change its role).
+#include <algorithm>
+
 #include "sa_device.h"
 #include "sa_internal.h"
 
 namespace sa {
 namespace {
 
-constexpr int kTile = 64;  // keys per LDS tile
+constexpr int kTile = 64;       // keys per LDS tile
+constexpr int kCusPerXcd = 32;  // MI355X: 8 XCDs of 32 CUs
 
 // Query blocks of every (b,h) pair ordered by kv_cnt descending, then by
 // block index ascending.
@@ -62,6 +65,58 @@ order_rows_kernel(const int32_t* __restrict__ kv_cnt, int32_t* __restrict__ orde
       rank += (o > mine) || (o == mine && j < r);
     }
     order[base + rank] = r;
+  }
+}
+
+// Launch schedule when the pair count is a multiple of 8.  Workgroup w runs
+// on XCD w % 8, which owns the pairs x, x+8, x+16, ...; entry i of XCD x's
+// list (pair << 11 | query block) is the work of its workgroup 8*i + x.  The
+// list holds first the full rows (lists of all n_b key blocks: the protected
+// query blocks) of every pair the XCD owns, pair by pair, then the other rows
+// pair by pair, each pair's rows in launch order (heaviest list first).  A
+// full row takes n_b / k_keep times as long as the others; started first, the
+// full rows of the XCD's last pairs no longer run alone at the end of the
+// launch, while the other rows still go through one pair at a time, so that
+// their K/V blocks are shared through the XCD's L2.
+__global__ void __launch_bounds__(1024)
+schedule_rows_kernel(const int32_t* __restrict__ kv_cnt, const int32_t* __restrict__ order,
+                     int32_t* __restrict__ sched, int* __restrict__ claim, int P, int n_b) {
+  __shared__ int nfull[kMaxPairs / 8 + 1];
+  __shared__ int total_full;
+  const int x = blockIdx.x, np = P >> 3, tid = threadIdx.x;
+  if (tid == 0) claim[64 * x] = 0;  // the attention kernel's row counter of XCD x
+  for (int j = 0; j < np; ++j) {
+    const size_t base = static_cast<size_t>(x + 8 * j) * n_b;
+    int nf = 0;
+    for (int r0 = 0; r0 < n_b; r0 += blockDim.x) {
+      const int r = r0 + tid;
+      nf += __syncthreads_count(r < n_b && kv_cnt[base + r] >= n_b);
+    }
+    if (tid == 0) nfull[j] = nf;
+  }
+  __syncthreads();
+  if (tid == 0) {  // exclusive prefix over the pairs, in pair order
+    int acc = 0;
+    for (int j = 0; j < np; ++j) {
+      const int nf = nfull[j];
+      nfull[j] = acc;
+      acc += nf;
+    }
+    nfull[np] = acc;
+    total_full = acc;
+  }
+  __syncthreads();
+  int32_t* out = sched + static_cast<size_t>(x) * np * n_b;
+  const int F = total_full;
+  for (int j = 0; j < np; ++j) {
+    const int pair = x + 8 * j;
+    const size_t base = static_cast<size_t>(pair) * n_b;
+    const int fpre = nfull[j], nf = nfull[j + 1] - fpre;
+    const int rest_pre = j * n_b - fpre;  // other rows of the earlier pairs
+    for (int rank = tid; rank < n_b; rank += blockDim.x) {
+      const int pos = rank < nf ? fpre + rank : F + rest_pre + (rank - nf);
+      out[pos] = (pair << 11) | order[base + rank];
+    }
   }
 }
 
@@ -104,9 +159,10 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
                         uint16_t* __restrict__ o, float* __restrict__ lse,
                         const int32_t* __restrict__ kv_idx,
                         const int32_t* __restrict__ kv_cnt,
-                        const int32_t* __restrict__ order, int P, int L,
-                        int n_b, float c, const int32_t* __restrict__ rows, int n_rows,
-                        int H, int n_split, float* __restrict__ part, int Lq) {
+                        const int32_t* __restrict__ order,
+                        const int32_t* __restrict__ sched, int* __restrict__ claim, int P,
+                        int L, int n_b, float c, const int32_t* __restrict__ rows,
+                        int n_rows, int H, int n_split, float* __restrict__ part, int Lq) {
   constexpr int NW = BLOCK / 32;             // waves per workgroup
   constexpr int TPB = BLOCK / kTile;         // tiles per key block
   constexpr int KC = D / 16;                 // k-steps of Q K^T
@@ -119,30 +175,62 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
   __shared__ __attribute__((aligned(1024))) uint16_t Ks[2][TILE_ELEMS];
   __shared__ __attribute__((aligned(1024))) uint16_t Vs[2][TILE_ELEMS];
   __shared__ uint16_t tiles[kMaxBlocks * TPB];  // valid tiles, as key0 / 64
-  __shared__ int ntiles_sh, nfull_sh;
+  __shared__ int ntiles_sh, nfull_sh, item_sh;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, n = lane & 31;
 
-  // Workgroup w runs on XCD w % 8.  When the pair count is a multiple of 8,
-  // XCD x works through its pairs x, x+8, ... one at a time, heaviest query
-  // block first: the K/V blocks of the pair in flight are shared through that
-  // XCD's L2, and only 8 pairs are live at once across the chip.
+  // Workgroup w runs on XCD w % 8.  Block lists with a pair count that is a
+  // multiple of 8: the workgroups are persistent, and those of XCD x take
+  // rows from x's launch list (its pairs' full rows, then its pairs one at a
+  // time, so that a pair's K/V blocks are shared through one L2) by an atomic
+  // counter per XCD; once that list is used up they take rows from the other
+  // XCDs' lists, which evens out XCDs that run at different speeds.  Each row
+  // is computed the same way whichever workgroup takes it.  Otherwise there
+  // is one workgroup per row (dense rows: XCD-major over pairs).
+  const bool persistent = !GATHER && (P & 7) == 0;
+  const int per_xcd = (P >> 3) * n_b;  // rows in each XCD's list (persistent form)
+  const int xcd = blockIdx.x & 7;
+  int exhausted = 0;                   // lists found empty (thread 0)
+  for (int item_iter = 0;; ++item_iter) {
   const int n_qr = GATHER ? ceil_div(n_rows, BLOCK) : n_b;  // query blocks per pair
   const int n_q = GATHER ? n_qr * n_split : n_b;              // workgroups per pair
-  int pair, rank;
-  if ((P & 7) == 0) {
-    const int i = blockIdx.x >> 3;
-    pair = (blockIdx.x & 7) + 8 * (i / n_q);
-    rank = i % n_q;
+  int pair, rank = 0, r = 0;
+  if (persistent) {
+    if (tid == 0) {
+      int item = -1;
+      for (int k = 0; k < 8 && item < 0; ++k) {
+        const int xq = (xcd + k) & 7;
+        if (exhausted & (1 << xq)) continue;
+        const int i = atomicAdd(claim + 64 * xq, 1);
+        if (i < per_xcd)
+          item = xq * per_xcd + i;
+        else
+          exhausted |= 1 << xq;
+      }
+      item_sh = item;
+    }
+    __syncthreads();
+    const int item = __builtin_amdgcn_readfirstlane(item_sh);  // uniform: scalar addressing
+    if (item < 0) break;
+    const int e = __builtin_amdgcn_readfirstlane(sched[item]);
+    pair = e >> 11;
+    r = e & 2047;
   } else {
-    pair = blockIdx.x % P;
-    rank = blockIdx.x / P;
+    if (item_iter > 0) break;
+    if (GATHER && (P & 7) == 0) {
+      const int i = blockIdx.x >> 3;
+      pair = (blockIdx.x & 7) + 8 * (i / n_q);
+      rank = i % n_q;
+    } else {
+      pair = blockIdx.x % P;
+      rank = blockIdx.x / P;
+    }
   }
   const size_t row_base = static_cast<size_t>(pair) * n_b;
-  int r, cnt, kb0 = 0, split = 0;
+  int cnt, kb0 = 0, split = 0;
   const int32_t* idx = nullptr;
   if constexpr (GATHER) {
     // consecutive ranks share a key run and so its K/V tiles in L2
@@ -151,7 +239,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     kb0 = n_b * split / n_split;
     cnt = n_b * (split + 1) / n_split - kb0;
   } else {
-    r = order[row_base + rank];
+    if (!persistent) r = order[row_base + rank];
     cnt = kv_cnt[row_base + r];
     cnt = cnt < 0 ? 0 : (cnt > n_b ? n_b : cnt);
     idx = kv_idx + (row_base + r) * n_b;
@@ -458,6 +546,36 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     kread(1, ka[1]);
     n0 = zero16();
     n1 = zero16();
+    // P(t) is formed in three stages a step apart, so that no instruction
+    // waits on the one just before it: in step st the FMAs of pair group
+    // st+1, the exponentials of group st, and the bf16 packing of group st-1
+    // (a group is the PPA pairs of one step; pair pk holds elements 2pk and
+    // 2pk+1 of S(t), from c0 for pk < 8, else from c1).
+    float fx[2][PPA][2], ex[2][PPA][2];
+    auto stage_fma = [&](int grp) {
+#pragma unroll
+      for (int u = 0; u < PPA; ++u) {
+        const int pk = grp * PPA + u;
+        const f32x16& src = pk < 8 ? c0 : c1;
+        const int e = 2 * (pk & 7);
+        fx[grp & 1][u][0] = fmaf(src[e], c, -m);
+        fx[grp & 1][u][1] = fmaf(src[e + 1], c, -m);
+      }
+    };
+    auto stage_exp = [&](int grp) {
+#pragma unroll
+      for (int u = 0; u < PPA; ++u) {
+        ex[grp & 1][u][0] = fast_exp2(fx[grp & 1][u][0]);
+        ex[grp & 1][u][1] = fast_exp2(fx[grp & 1][u][1]);
+        if constexpr (GATHER) lsum += ex[grp & 1][u][0] + ex[grp & 1][u][1];  // fp32 row sum
+      }
+    };
+    auto stage_pack = [&](int grp) {
+#pragma unroll
+      for (int u = 0; u < PPA; ++u)
+        pb[grp * PPA + u] = pack_bf16x2(ex[grp & 1][u][0], ex[grp & 1][u][1]);
+    };
+    stage_fma(0);
 #pragma unroll
     for (int st = 0; st < NA; ++st) {
       const int kc = st >> 1;
@@ -466,25 +584,25 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
         n1 = mfma32x32x16(ka[kc % 3][1], qf[kc], n1);
       else
         n0 = mfma32x32x16(ka[kc % 3][0], qf[kc], n0);
+      if (st > 0) stage_pack(st - 1);
+      stage_exp(st);
+      if (st + 1 < NA) stage_fma(st + 1);
 #pragma unroll
-      for (int u = 0; u < PPA; ++u) {
-        const int pk = st * PPA + u;  // 0..7 from c0, 8..15 from c1
-        const f32x16& src = pk < 8 ? c0 : c1;
-        const int e = 2 * (pk & 7);
-        const float pa = fast_exp2(fmaf(src[e], c, -m));
-        const float pc = fast_exp2(fmaf(src[e + 1], c, -m));
-        pb[pk] = pack_bf16x2(pa, pc);
-        if constexpr (GATHER) lsum += pa + pc;  // fp32 row sum (exact lse)
-      }
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
+      for (int i = 0; i < NI; ++i) {
         if (i * NA / NI == st) {
           const uint32_t la = (uint32_t)(size_t)(lds_void_t*)kdst;
           lds_dma16(kbase, dma_full[i],
                     __builtin_amdgcn_readfirstlane(la + (wave_u + NW * i) * 1024));
         }
+        if (i * NA / NI + NA / (2 * NI) == st) {
+          const uint32_t la = (uint32_t)(size_t)(lds_void_t*)vdst;
+          lds_dma16(vbase, dma_full[i],
+                    __builtin_amdgcn_readfirstlane(la + (wave_u + NW * i) * 1024));
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
+    stage_pack(NA - 1);
     // ---- PV phase: O^T += V(t)^T P(t)^T; row sums of P(t), row max of S(t+1)
     __builtin_amdgcn_s_setprio(0);
     constexpr int NB = 4 * DT;          // MFMAs
@@ -515,13 +633,6 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
           asm volatile("" : "+v"(mxn));  // keeps this share of the max in its slot
         }
       }
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
-        if (i * NB / NI == j) {
-          const uint32_t la = (uint32_t)(size_t)(lds_void_t*)vdst;
-          lds_dma16(vbase, dma_full[i],
-                    __builtin_amdgcn_readfirstlane(la + (wave_u + NW * i) * 1024));
-        }
       __builtin_amdgcn_sched_barrier(0);
     }
     mx_cur = mxn;
@@ -585,6 +696,7 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
       lse[static_cast<size_t>(pair) * LQ + qrow] =
           ltot > 0.f ? (m + __log2f(ltot)) * kLn2 : -INFINITY;
   }
+  }  // next row
 }
 
 // Merges the n_split partial rows of each gathered query (rows[b*n_rows + j],
@@ -728,24 +840,33 @@ void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
   const int P = B * H;
   const AttnWs lay = attn_ws_layout(B, H, n_b, d, block);
   int32_t* order = reinterpret_cast<int32_t*>(ws + lay.order);
+  int32_t* sched = reinterpret_cast<int32_t*>(ws + lay.sched);
+  int* claim = reinterpret_cast<int*>(ws + lay.claim);
   const float c = scale * kLog2e;
   hipLaunchKernelGGL(order_rows_kernel, dim3(P), dim3(256), 0, s, kv_cnt, order, n_b);
-  const dim3 grid(P * n_b);
+  // pair count a multiple of 8: persistent workgroups, as many as the chip
+  // holds at once (2 per CU, 32 CUs per XCD) and no more than the rows
+  dim3 grid(P * n_b);
+  if ((P & 7) == 0) {
+    hipLaunchKernelGGL(schedule_rows_kernel, dim3(8), dim3(1024), 0, s, kv_cnt, order, sched,
+                       claim, P, n_b);
+    grid = dim3(8 * std::min((P >> 3) * n_b, 2 * kCusPerXcd));
+  }
   if (d == 128 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 128, false>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, sched, claim, P, L, n_b, c, nullptr, 0, H, 1,
                        nullptr, L);
   else if (d == 128 && block == 64)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, 64, false>), grid, dim3(128), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, sched, claim, P, L, n_b, c, nullptr, 0, H, 1,
                        nullptr, L);
   else if (d == 64 && block == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 128, false>), grid, dim3(256), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, sched, claim, P, L, n_b, c, nullptr, 0, H, 1,
                        nullptr, L);
   else
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, 64, false>), grid, dim3(128), 0, s,
-                       q, k, v, o, lse, kv_idx, kv_cnt, order, P, L, n_b, c, nullptr, 0, H, 1,
+                       q, k, v, o, lse, kv_idx, kv_cnt, order, sched, claim, P, L, n_b, c, nullptr, 0, H, 1,
                        nullptr, L);
 }
 
@@ -780,11 +901,11 @@ void launch_gather_attention_bf16(const uint16_t* q, const uint16_t* k, const ui
   const dim3 grid(P * ceil_div(n_rows, kTokRowBlock) * ns);
   if (d == 128)
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<128, kTokRowBlock, true>), grid, dim3(256), 0,
-                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, Lk, n_b, c, rows,
+                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, nullptr, nullptr, P, Lk, n_b, c, rows,
                        n_rows, H, ns, part, Lq);
   else
     hipLaunchKernelGGL((sparse_attn_bf16_kernel<64, kTokRowBlock, true>), grid, dim3(256), 0,
-                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, P, Lk, n_b, c, rows,
+                       s, q, k, v, o, lse, nullptr, nullptr, nullptr, nullptr, nullptr, P, Lk, n_b, c, rows,
                        n_rows, H, ns, part, Lq);
   if (ns > 1) {
     const size_t threads = static_cast<size_t>(P) * n_rows * (d / 4);

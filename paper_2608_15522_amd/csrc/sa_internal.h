@@ -74,6 +74,8 @@ inline MaskWs mask_ws_layout(int B, int H, int n_b, int d) {
 
 struct AttnWs {
   size_t order;   // int [B,H,n_b]  query blocks of each head, heaviest first
+  size_t sched;   // int [8][B*H/8][n_b]  per-XCD launch list (B*H a multiple of 8)
+  size_t claim;   // int [8][64]  rows taken from each XCD's list (one per 256 bytes)
   size_t total;
 };
 
@@ -81,6 +83,8 @@ inline AttnWs attn_ws_layout(int B, int H, int n_b, int /*d*/, int /*block*/) {
   AttnWs w{};
   size_t off = 0;
   w.order = off; off += align_up(sizeof(int32_t) * B * H * n_b);
+  w.sched = off; off += align_up(sizeof(int32_t) * B * H * n_b);
+  w.claim = off; off += align_up(sizeof(int32_t) * 8 * 64);
   w.total = off;
   return w;
 }

@@ -64,7 +64,7 @@ def test_workspace_sizes():
         assert 0 < a < b
     # attention: the per-head launch order of the query blocks (int32)
     assert sa.sa_workspace_size(sa.SA_CALL_SPARSE_ATTENTION, 1, 24, 32760, 512,
-                                128, 128) == 24 * 256 * 4
+                                128, 128) == 2 * 24 * 256 * 4 + 8 * 64 * 4
     assert sa.sa_workspace_size(sa.SA_CALL_SELECT_PROTECTED, 1, 1, 10, 1, 64, 64) == 0
     for bad in [(0, 1, 10, 1, 64, 64), (1, 1, 10, 1, 96, 64),
                 (1, 1, 10, 1, 64, 32), (1, 1, 2049 * 128, 1, 64, 128)]:
@@ -262,7 +262,7 @@ INVALID = [
     (_attn_na, dict(q=None), sa.SA_ERR_INVALID_ARG, "q is NULL"),
     (_attn_na, dict(kv_cnt=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
     (_attn_na, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
-    # B*H*n_b = 600 * 2048 entries of launch order exceed the 4 MiB scratch
+    # B*H*n_b = 600 * 2048 entries of launch order and schedule exceed the 4 MiB scratch
     (_attn_na, dict(H=600, L=262144), sa.SA_ERR_UNSUPPORTED, "scratch"),
     (_mask, dict(k_keep=0), sa.SA_ERR_INVALID_ARG, "k_keep"),
     (_mask, dict(k_keep=9), sa.SA_ERR_INVALID_ARG, "k_keep"),
