@@ -74,7 +74,7 @@ constexpr int kMaxPoolBlock = 128;  // largest supported block
 // [d][n_pad]) = mean of the rows of block c, in fp64: the sums of bf16 or
 // fp32 inputs are exact, the mean is rounded once.  Per block, thread
 // (rg, cc) loads 16-byte chunk cc of rows rg, rg + RG, ... of both matrices
-// (every load issued before the first sum) and the RG partial sums of each
+// (issued while the previous block is summed) and the RG partial sums of each
 // element are added in a fixed order; the means of the workgroup's blocks
 // are written as runs of consecutive columns.
 constexpr int kPoolBlocks = 8;  // blocks per block_pool workgroup
@@ -94,20 +94,27 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
   const size_t pair = blockIdx.y;
   const int nblk = min(kPoolBlocks, n_b - c0);
   const int cc = threadIdx.x % CPR, rg = threadIdx.x / CPR;
-  for (int j = 0; j < nblk; ++j) {
+  // the rows of block j+1 are loaded while block j is summed
+  auto load_block = [&](int j, u32x4 (&dst)[2][NR]) {
     const int row0 = (c0 + j) * block;
-    const int len = min(block, L - row0);
-    u32x4 raw[2][NR];
+    const int len = j < nblk ? min(block, L - row0) : 0;
 #pragma unroll
     for (int which = 0; which < 2; ++which) {
       const T* src = (which == 0 ? q : k) + pair * L * D;
 #pragma unroll
       for (int i = 0; i < NR; ++i) {
         const int r = rg + RG * i;
-        raw[which][i] = r < len ? ldg16(src + static_cast<size_t>(row0 + r) * D + cc * EPC)
+        dst[which][i] = r < len ? ldg16(src + static_cast<size_t>(row0 + r) * D + cc * EPC)
                                 : u32x4{0u, 0u, 0u, 0u};
       }
     }
+  };
+  u32x4 raw[2][NR], nxt[2][NR];
+  load_block(0, raw);
+  for (int j = 0; j < nblk; ++j) {
+    const int row0 = (c0 + j) * block;
+    const int len = min(block, L - row0);
+    load_block(j + 1, nxt);
     __syncthreads();  // the previous block's partial sums have been read
 #pragma unroll
     for (int which = 0; which < 2; ++which) {
@@ -132,6 +139,10 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
       for (int i = 0; i < RG; ++i) sum += part[which][i][dd % EPC][dd / EPC];
       mean[which][dd][j] = sum / static_cast<double>(len);
     }
+#pragma unroll
+    for (int which = 0; which < 2; ++which)
+#pragma unroll
+      for (int i = 0; i < NR; ++i) raw[which][i] = nxt[which][i];
   }
   __syncthreads();
   for (int t = threadIdx.x; t < 2 * D * kPoolBlocks; t += 256) {
@@ -144,8 +155,12 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
 }
 
 // ---- K6 ---------------------------------------------------------------------
-constexpr int kMaskWaves = 4;
-constexpr int kMaskThreads = kMaskWaves * 64;
+// Waves per mask workgroup: a divisor of E (the 64-column groups of a row)
+// from 4 up, so that every wave computes the scores of as many groups; 4
+// when E is below 4 or has no such divisor up to 8.
+__host__ __device__ constexpr int mask_waves(int E) {
+  return E < 4 ? 4 : (E % 4 == 0 ? 4 : (E % 5 == 0 ? 5 : (E % 6 == 0 ? 6 : 4)));
+}
 
 // Query-block rows per mask workgroup: the row exchange holds rows x n_pad
 // doubles in at most 64 KB of LDS, and from n_pad = 1280 on fewer rows keep
@@ -188,23 +203,26 @@ __device__ __forceinline__ void wave_kth_prefix(const uint64_t* keys, int k, uin
 // takes (b,h) pair (w % 8) + 8 * ((w / 8) / nrt) and row tile (w / 8) % nrt,
 // so all tiles of a pair share one XCD's L2 (workgroups past P exit).
 // Pooled means are [d][n_pad] per (b,h).  Phase 1: the workgroup's R query
-// rows are copied to LDS as [d][R]; wave w computes G = scale * qbar kbar^T
-// for them and the 64-column groups w, w+4, ... with one column per lane: the
+// rows are copied to LDS as [d][R]; wave w of W (mask_waves(E)) computes
+// G = scale * qbar kbar^T for them and the 64-column groups w, w+W, ... with
+// one column per lane: the
 // lane's key values are loaded KP d-steps ahead into registers and each feeds
 // R fp64 FMAs whose query operands are LDS reads shared by the whole wave.
 // Rows >= n_b and columns >= n_b read padding and are discarded.  Phase 2:
-// the rows go through LDS; wave w takes rows w, w+4, ... with column
+// the rows go through LDS; wave w takes rows w, w+W, ... with column
 // col = 64*e + lane in register e of lane `lane`, and either emits the full
 // list (protected row) or the top-k_keep blocks.
 template <int D, int E>
-__global__ void __launch_bounds__(kMaskThreads)
+__global__ void __launch_bounds__(64 * mask_waves(E))
 mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kbar,
                   const uint8_t* __restrict__ prot_flag, int H, int n_b, int k_keep,
                   double scale, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt,
                   uint8_t* __restrict__ mask, float* __restrict__ scores, int P) {
   constexpr int NPAD = 64 * E;
   constexpr int R = mask_rows_per_wg(E);
-  constexpr int KP = E >= 5 ? 16 : 32;  // d-steps of key values in flight per lane
+  constexpr int kMaskWaves = mask_waves(E);
+  constexpr int kMaskThreads = 64 * kMaskWaves;
+  constexpr int KP = E >= 5 ? 8 : 32;  // d-steps of key values in flight per lane (registers)
   constexpr int CUNR = E >= 5 ? 1 : 2;   // chunk pairs unrolled (register budget)
   static_assert(D % (2 * KP) == 0 && R % 2 == 0, "chunking");
   __shared__ double gs[R][NPAD];
@@ -233,6 +251,8 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
 #pragma unroll
       for (int j = 0; j < KP; ++j) kv[j] = kp[static_cast<size_t>(c * KP + j) * NPAD + col];
     };
+    // the query means of a d-step are read just ahead of their FMAs: hoisting
+    // a whole chunk's reads would hold KP * R doubles in registers
     auto use_chunk = [&](const double* kv, int c) {
 #pragma unroll
       for (int j = 0; j < KP; ++j) {
@@ -242,6 +262,9 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
           const double2 qq = *reinterpret_cast<const double2*>(qrow + i);
           acc[i] = fma(qq.x, kv[j], acc[i]);
           acc[i + 1] = fma(qq.y, kv[j], acc[i + 1]);
+        }
+        if constexpr (E >= 5) {
+          if (j % 2 == 1) __builtin_amdgcn_sched_barrier(0);
         }
       }
     };
@@ -307,7 +330,8 @@ void launch_mask_build(int E, dim3 grid, hipStream_t s, const double* qbar,
                        uint8_t* mask, float* scores) {
 #define SA_MASK_CASE(EV)                                                                 \
   case EV:                                                                               \
-    hipLaunchKernelGGL((mask_build_kernel<D, EV>), grid, dim3(kMaskThreads), 0, s, qbar,  \
+    hipLaunchKernelGGL((mask_build_kernel<D, EV>), grid, dim3(64 * mask_waves(EV)), 0, s,  \
+                       qbar,                                                              \
                        kbar, prot_flag, H, n_b, k_keep, sc, kv_idx, kv_cnt, mask, scores, \
                        P);                                                                \
     break;
