@@ -44,8 +44,6 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="ovi_bf16")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-heads", type=int, default=3,
-                   help="heads of the layer the oracle is timed on")
     p.add_argument("--dense-steps", type=int, default=5)
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
                    help="run one device-to-device copy of this many MiB before "
@@ -407,27 +405,62 @@ def time_attention(plan, t, kv_idx, kv_cnt, steps, torch, sa):
     return e0.elapsed_time(e1) / steps
 
 
-def cpu_baseline(w, x, kv_idx, kv_cnt, heads):
-    """The oracle as it stands, timed on `heads` heads of the layer (every
-    step is per head, so the full-layer time is the sample scaled by H/heads).
-    Returns the dict of the report."""
+# Inputs of the CPU baseline, set before the worker pool is forked so that the
+# workers share them (copy-on-write) and never hold any GPU state.
+_CPU_X = None
+
+
+def _cpu_pool_init():
+    try:
+        from threadpoolctl import threadpool_limits
+        threadpool_limits(1)  # one BLAS thread per worker
+    except Exception:  # pragma: no cover
+        pass
+
+
+def _cpu_head(task):
+    """The oracle's steps for one (b, h) slab of the layer: the a->v and v->a
+    saliency of that head, its pooled-QK block mask and its sparse attention
+    on the GPU's lists.  Returns the seconds it took."""
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        cores = 1
-    hs = slice(0, heads)
-    sub = {k: x[k][:, hs] for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
+    b, h, scale, block, k_keep, n_b, kv_idx_bh, kv_cnt_bh = task
+    x = _CPU_X
+    sl = lambda k: x[k][b:b + 1, h:h + 1]
     t0 = time.perf_counter()
-    oracle.cross_scores(sub["q_a"], sub["k_v"], w.scale, sub["q_v"], sub["k_a"])
-    prot = np.zeros((w.B, w.n_b), dtype=np.uint8)
-    oracle.block_mask(sub["q_v"], sub["k_v"], w.scale, w.block, w.k_keep, prot)
-    oracle.masked_attention(sub["q_v"], sub["k_v"], sub["v_v"], w.scale, w.block,
-                            kv_idx[:, hs], kv_cnt[:, hs])
-    dt = time.perf_counter() - t0
-    layer_s = dt * w.H / heads
+    oracle.cross_scores(sl("q_a"), sl("k_v"), scale, sl("q_v"), sl("k_a"))
+    oracle.block_mask(sl("q_v"), sl("k_v"), scale, block, k_keep,
+                      np.zeros((1, n_b), dtype=np.uint8))
+    oracle.masked_attention(sl("q_v"), sl("k_v"), sl("v_v"), scale, block,
+                            kv_idx_bh[None, None], kv_cnt_bh[None, None])
+    return time.perf_counter() - t0
+
+
+def cpu_workers():
+    """Worker count: the CPUs this process may run on, at most 16 (the host
+    share of one GPU)."""
+    return max(1, min(len(os.sched_getaffinity(0)), 16))
+
+
+def make_cpu_pool(x):
+    """Fork the worker pool of the CPU baseline; called before torch touches
+    the GPU."""
+    import multiprocessing as mp
+    global _CPU_X
+    _CPU_X = x
+    return mp.get_context("fork").Pool(cpu_workers(), initializer=_cpu_pool_init)
+
+
+def cpu_baseline(w, pool, kv_idx, kv_cnt):
+    """The oracle as it stands, timed on the whole layer: every (b, h) slab on
+    a pool of worker processes with one BLAS thread each.  Returns the dict
+    of the report."""
+    import numpy as np
+    tasks = [(b, h, w.scale, w.block, w.k_keep, w.n_b, np.ascontiguousarray(kv_idx[b, h]),
+              np.ascontiguousarray(kv_cnt[b, h])) for b in range(w.B) for h in range(w.H)]
+    t0 = time.perf_counter()
+    per_head = pool.map(_cpu_head, tasks, chunksize=1)
+    layer_s = time.perf_counter() - t0
     dense = 4.0 * w.B * w.H * w.L_v ** 2 * w.d
     cpu_model = "unknown"
     try:
@@ -437,12 +470,14 @@ def cpu_baseline(w, x, kv_idx, kv_cnt, heads):
     except OSError:  # pragma: no cover
         pass
     return {"value": round(dense / layer_s / 1e12, 6), "unit": "TFLOP/s",
-            "cores": int(cores), "kind": "oracle", "cpu_model": cpu_model,
-            "numpy": np.__version__,
+            "cores": cpu_workers(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "kind": "oracle", "cpu_model": cpu_model, "numpy": np.__version__,
             "ms_per_layer": round(layer_s * 1e3, 1),
-            "sample": (f"{heads} of {w.H} heads of the {w.name} layer (saliency in "
-                       f"both directions, pooled-QK block mask, sparse attention on "
-                       f"the GPU's lists), {dt:.1f} s, scaled by {w.H}/{heads}")}
+            "cpu_seconds": round(float(sum(per_head)), 1),
+            "sample": (f"the whole {w.name} layer: {w.B * w.H} (b, h) slabs, each the "
+                       f"saliency in both directions, the pooled-QK block mask and the "
+                       f"sparse attention on the GPU's lists, on {cpu_workers()} worker "
+                       f"processes with one BLAS thread each")}
 
 
 def run_sweep(path, steps, torch, sa, synth, LayerPlan):
@@ -489,16 +524,18 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import numpy as np
-    import torch
     import synth
-    import paper_2608_15522_amd as sa
-    from paper_2608_15522_amd.layer import LayerPlan
 
     w = synth.WORKLOADS[args.workload]
     print(f"bench: {w.name} B={w.B} H={w.H} L_v={w.L_v} L_a={w.L_a} d={w.d} "
           f"block={w.block} k_keep={w.k_keep} k_prot={w.k_prot}", file=sys.stderr,
           flush=True)
     x = synth.make_inputs(w)
+    # the oracle's worker pool is forked before the GPU is initialised
+    pool = None if args.no_cpu_baseline else make_cpu_pool(x)
+    import torch
+    import paper_2608_15522_amd as sa
+    from paper_2608_15522_amd.layer import LayerPlan
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     t = {k: torch.from_numpy(x[k]).to(dt).cuda() for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
     plan = LayerPlan(w.B, w.H, w.L_v, w.L_a, w.d, w.block, w.k_keep, w.k_prot, w.scale,
@@ -612,7 +649,9 @@ def main():
     if not args.no_cpu_baseline:
         del t
         torch.cuda.empty_cache()
-        res["cpu_baseline"] = cpu_baseline(w, x, kv_idx, kv_cnt, min(args.cpu_heads, w.H))
+        res["cpu_baseline"] = cpu_baseline(w, pool, kv_idx, kv_cnt)
+        pool.close()
+        pool.join()
     print(json.dumps(res), flush=True)
 
 
