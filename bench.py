@@ -34,7 +34,8 @@ PEAK_HBM_GBS = 8000.0
 ATTN_KERNEL = "sparse_attn_bf16_kernel<128,128,false>"
 ATTN_SOURCES = ("paper_2608_15522_amd/csrc/sa_attn.hip",
                 "paper_2608_15522_amd/csrc/sa_device.h")
-TRAFFIC_FILE = "profiles/ovi_layer_hbm_bytes.md"
+# Counter summaries per workload: profiles/<prefix>_layer_hbm_bytes.md.
+TRAFFIC_FILES = {"ovi_bf16": "ovi", "ltx_bf16": "ltx", "long_cfg_bf16": "long_cfg"}
 
 
 def parse():
@@ -83,8 +84,11 @@ def attention_traffic(workload):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     src = h.hexdigest()[:16]
+    if workload not in TRAFFIC_FILES:
+        return None, None
+    path = "profiles/%s_layer_hbm_bytes.md" % TRAFFIC_FILES[workload]
     try:
-        text = open(os.path.join(ROOT, TRAFFIC_FILE)).read()
+        text = open(os.path.join(ROOT, path)).read()
     except OSError:
         return None, None
     for line in text.splitlines():
@@ -93,7 +97,7 @@ def attention_traffic(workload):
         kv = dict(f.split("=", 1) for f in line.split()[1:])
         if (kv.get("kernel") == ATTN_KERNEL and kv.get("workload") == workload
                 and kv.get("src") == src):
-            return int(kv["fetch_bytes"]) + int(kv["write_bytes"]), TRAFFIC_FILE
+            return int(kv["fetch_bytes"]) + int(kv["write_bytes"]), path
     return None, None
 
 
