@@ -8,15 +8,16 @@
 //    over the valid tokens of each block, accumulated in fp64 (16-byte loads,
 //    fixed-order LDS reduction; the sums of bf16/fp32 inputs are exact),
 //    stored as [d][n_pad] (block index innermost).
-// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 8 or 4 query
-//    blocks (4 for the widest rows; rows padded to 64 * E columns),
-//    the pooled scores G = scale * qbar kbar^T by fp64 FMA (a few hundred
-//    MFLOP per layer; fp32 would misrank scores closer than ~1e-6, and
-//    pooled-score gaps are that small), then per row either the full list
-//    (protected row) or the top-k_keep blocks: one wave finds the k-th
-//    smallest order key (value descending, index ascending) by a bitwise
-//    search with ballots and compacts the blocks at or below it into an
-//    ascending list.
+// K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 16 query blocks
+//    (rows padded to 64 * E columns, E <= 10; 8 or 4 blocks for wider
+//    rows), the pooled scores G = scale * qbar kbar^T in fp64, on the
+//    matrix cores (v_mfma_f64_16x16x4f64) up to 640 columns and by vector
+//    FMAs beyond (a few GFLOP per layer; fp32 would misrank scores closer
+//    than ~1e-6, and pooled-score gaps are that small), then per row
+//    either the full list (protected row) or the top-k_keep blocks: one
+//    wave finds the k-th smallest order key (value descending, index
+//    ascending) by a bitwise search with ballots and compacts the blocks at
+//    or below it into an ascending list.
 #include "sa_device.h"
 #include "sa_internal.h"
 
@@ -74,9 +75,9 @@ constexpr int kMaxPoolBlock = 128;  // largest supported block
 // [d][n_pad]) = mean of the rows of block c, in fp64: the sums of bf16 or
 // fp32 inputs are exact, the mean is rounded once.  Per block, thread
 // (rg, cc) loads 16-byte chunk cc of rows rg, rg + RG, ... of both matrices
-// (issued while the previous block is summed) and the RG partial sums of each
-// element are added in a fixed order; the means of the workgroup's blocks
-// are written as runs of consecutive columns.
+// and the RG partial sums of each element are added in a fixed order; the
+// means of the workgroup's blocks are written as runs of consecutive
+// columns.
 constexpr int kPoolBlocks = 8;  // blocks per block_pool workgroup
 
 template <typename T, int D>
@@ -94,7 +95,10 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
   const size_t pair = blockIdx.y;
   const int nblk = min(kPoolBlocks, n_b - c0);
   const int cc = threadIdx.x % CPR, rg = threadIdx.x / CPR;
-  // the rows of block j+1 are loaded while block j is summed
+  // One block in registers at a time: at 110 VGPRs three workgroups share a
+  // CU (as many as the LDS holds) and hide each other's loads; a second
+  // buffer for block j+1 took 174 VGPRs, two workgroups per CU, and left the
+  // 768-workgroup Ovi-like grid 1.5 rounds long (90 against 81 us).
   auto load_block = [&](int j, u32x4 (&dst)[2][NR]) {
     const int row0 = (c0 + j) * block;
     const int len = j < nblk ? min(block, L - row0) : 0;
@@ -109,12 +113,11 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
       }
     }
   };
-  u32x4 raw[2][NR], nxt[2][NR];
-  load_block(0, raw);
+  u32x4 raw[2][NR];
   for (int j = 0; j < nblk; ++j) {
     const int row0 = (c0 + j) * block;
     const int len = min(block, L - row0);
-    load_block(j + 1, nxt);
+    load_block(j, raw);
     __syncthreads();  // the previous block's partial sums have been read
 #pragma unroll
     for (int which = 0; which < 2; ++which) {
@@ -139,10 +142,6 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
       for (int i = 0; i < RG; ++i) sum += part[which][i][dd % EPC][dd / EPC];
       mean[which][dd][j] = sum / static_cast<double>(len);
     }
-#pragma unroll
-    for (int which = 0; which < 2; ++which)
-#pragma unroll
-      for (int i = 0; i < NR; ++i) raw[which][i] = nxt[which][i];
   }
   __syncthreads();
   for (int t = threadIdx.x; t < 2 * D * kPoolBlocks; t += 256) {
@@ -155,20 +154,26 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
 }
 
 // ---- K6 ---------------------------------------------------------------------
-// Waves per mask workgroup: a divisor of E (the 64-column groups of a row)
-// from 4 up, so that every wave computes the scores of as many groups; 4
-// when E is below 4 or has no such divisor up to 8.
+// Row widths up to 640 columns compute G on the matrix cores
+// (v_mfma_f64_16x16x4f64, fp64 products and sums like the vector path);
+// wider rows use fp64 FMAs on the vector ALUs.
+__host__ __device__ constexpr bool mask_uses_mfma(int E) { return E <= 10; }
+
+// Waves per mask workgroup.  Matrix-core path: 8, which with at most 113
+// VGPRs lets two 16-row workgroups share a CU (at 5 waves and 144 VGPRs a CU
+// held one, and the n_b = 591 mask took 290 instead of 205 us; at 8 waves
+// 153 us).  Vector path: a divisor of E from 4 up, so that every wave
+// computes the scores of as many 64-column groups; 4 when E has no such
+// divisor up to 6.
 __host__ __device__ constexpr int mask_waves(int E) {
-  return E < 4 ? 4 : (E % 4 == 0 ? 4 : (E % 5 == 0 ? 5 : (E % 6 == 0 ? 6 : 4)));
+  return mask_uses_mfma(E) ? 8 : (E % 4 == 0 ? 4 : (E % 5 == 0 ? 5 : (E % 6 == 0 ? 6 : 4)));
 }
 
-// Query-block rows per mask workgroup: the row exchange holds rows x n_pad
-// doubles in at most 64 KB of LDS, and from n_pad = 1280 on fewer rows keep
-// phase 1 within the register budget.  Below that, 8 rows rather than 16
-// give twice the workgroups and hide more of the key-mean loads (10 % less
-// time at n_b = 256).
+// Query-block rows per mask workgroup: 16 on the matrix-core path (its tile
+// height; the rows of G fill at most 80 KB of LDS); on the vector path 8,
+// and 4 from n_pad = 1280 on, where the rows would not fit otherwise.
 __host__ __device__ constexpr int mask_rows_per_wg(int E) {
-  return E >= 20 ? 4 : 8;
+  return mask_uses_mfma(E) ? 16 : (E >= 20 ? 4 : 8);
 }
 
 // k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 distinct
@@ -198,35 +203,49 @@ __device__ __forceinline__ void wave_kth_prefix(const uint64_t* keys, int k, uin
   }
 }
 
-// 1-D grid of 8 * ceil(P / 8) * ceil(n_b / R) workgroups, 4 waves; template
-// E = n_pad / 64.  Workgroup w runs on XCD w % 8 (round-robin dispatch) and
-// takes (b,h) pair (w % 8) + 8 * ((w / 8) / nrt) and row tile (w / 8) % nrt,
-// so all tiles of a pair share one XCD's L2 (workgroups past P exit).
-// Pooled means are [d][n_pad] per (b,h).  Phase 1: the workgroup's R query
-// rows are copied to LDS as [d][R]; wave w of W (mask_waves(E)) computes
-// G = scale * qbar kbar^T for them and the 64-column groups w, w+W, ... with
-// one column per lane: the
-// lane's key values are loaded KP d-steps ahead into registers and each feeds
-// R fp64 FMAs whose query operands are LDS reads shared by the whole wave.
-// Rows >= n_b and columns >= n_b read padding and are discarded.  Phase 2:
-// the rows go through LDS; wave w takes rows w, w+W, ... with column
-// col = 64*e + lane in register e of lane `lane`, and either emits the full
-// list (protected row) or the top-k_keep blocks.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource over n_bytes from base (gfx9 raw buffer, bounds-checked:
+// loads past n_bytes return 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const double* base, int n_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<double*>(base), 0, n_bytes, 0x00020000);
+}
+__device__ __forceinline__ double buffer_load_f64(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+
+// 1-D grid of 8 * ceil(P / 8) * ceil(n_b / R) workgroups of mask_waves(E)
+// waves; template E = n_pad / 64.  Workgroup w runs on XCD w % 8
+// (round-robin dispatch) and takes (b,h) pair (w % 8) + 8 * ((w / 8) / nrt)
+// and row tile (w / 8) % nrt, so all tiles of a pair share one XCD's L2
+// (workgroups past P exit).  Pooled means are [d][n_pad] per (b,h).
+// Phase 1, the rows r0 .. r0+R-1 of G = scale * qbar kbar^T into LDS:
+//  * matrix-core path (R = 16): wave w takes the pairs of 16-column tiles
+//    w, w+W, ...; per 4 d-steps one A fragment (query means) and one B
+//    fragment per tile come from global memory, PD steps ahead, and each
+//    tile takes one v_mfma_f64_16x16x4f64.  Tiles past n_pad are skipped.
+//  * vector path: the workgroup's query means are copied to LDS as [d][R];
+//    wave w takes the 64-column groups w, w+W, ..., one column per lane: the
+//    lane's key means are loaded KP d-steps ahead and each feeds R fp64 FMAs
+//    whose query operands are broadcast LDS reads.
+// Rows >= n_b and columns >= n_b hold padding and are discarded.  Phase 2:
+// wave w takes rows w, w+W, ... with column col = 64*e + lane in register e
+// of lane `lane`, and either emits the full list (protected row) or the
+// top-k_keep blocks.
 template <int D, int E>
-__global__ void __launch_bounds__(64 * mask_waves(E))
+__global__ void __launch_bounds__(64 * mask_waves(E)) __attribute__((amdgpu_waves_per_eu(4)))
 mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kbar,
                   const uint8_t* __restrict__ prot_flag, int H, int n_b, int k_keep,
                   double scale, int32_t* __restrict__ kv_idx, int32_t* __restrict__ kv_cnt,
                   uint8_t* __restrict__ mask, float* __restrict__ scores, int P) {
   constexpr int NPAD = 64 * E;
+  constexpr bool MF = mask_uses_mfma(E);
   constexpr int R = mask_rows_per_wg(E);
   constexpr int kMaskWaves = mask_waves(E);
   constexpr int kMaskThreads = 64 * kMaskWaves;
-  constexpr int KP = E >= 5 ? 8 : 32;  // d-steps of key values in flight per lane (registers)
-  constexpr int CUNR = E >= 5 ? 1 : 2;   // chunk pairs unrolled (register budget)
-  static_assert(D % (2 * KP) == 0 && R % 2 == 0, "chunking");
-  __shared__ double gs[R][NPAD];
-  __shared__ __attribute__((aligned(16))) double qs[D][R];
+  // rows of G, then (vector path) the query means as [d][R]
+  __shared__ __attribute__((aligned(16))) double lds[R * NPAD + (MF ? 0 : D * R)];
+  double(*gs)[NPAD] = reinterpret_cast<double(*)[NPAD]>(lds);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nrt = ceil_div(n_b, R);
   const int wg = blockIdx.x;
@@ -237,48 +256,93 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
   const int r0 = ((wg / 8) % nrt) * R;
   const double* qp = qbar + pair * D * NPAD + r0;
   const double* kp = kbar + pair * D * NPAD;
+  const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(kp, D * NPAD * 8);
 
-  for (int i = tid; i < D * R; i += kMaskThreads) qs[i / R][i % R] = qp[(i / R) * NPAD + i % R];
-  __syncthreads();
+  if constexpr (MF) {
+    // A[i][kk] (query block r0+i, d = 4k+kk) sits in lane i + 16kk, B[kk][j]
+    // (d = 4k+kk, key block c0+j) in lane j + 16kk, and D[i][j] in lane
+    // j + 16(i % 4), element i / 4.
+    const __amdgpu_buffer_rsrc_t qrs = buffer_rsrc(qp, (D * NPAD - r0) * 8);
+    const int lo = lane & 15, hi = lane >> 4;
+    const int frag = (hi * NPAD + lo) * 8;  // byte offset of the lane's element in a 4-d slab
+    constexpr int KS = D / 4;               // k-steps
+    constexpr int PD = 4;                   // k-steps of fragments in flight
+    constexpr int TG = 2;                   // 16-column tiles per pass of a wave
+    constexpr int T = NPAD / 16;
+    constexpr int NG = T / TG;
 #pragma unroll 1
-  for (int cg = wave; cg < E; cg += kMaskWaves) {
-    const int col = 64 * cg + lane;
-    double acc[R];
+    for (int g = wave; g < NG; g += kMaskWaves) {
+      const int c0 = 16 * TG * g;
+      f64x4 acc[TG];
 #pragma unroll
-    for (int i = 0; i < R; ++i) acc[i] = 0.0;
-    // key values of chunk c (KP d-steps) alternate between ka and kb
-    auto load_chunk = [&](double* kv, int c) {
+      for (int t = 0; t < TG; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
+      double aq[PD], bq[PD][TG];
+      auto load_ab = [&](int k) {
+        aq[k % PD] = buffer_load_f64(qrs, frag, 4 * k * NPAD * 8);
 #pragma unroll
-      for (int j = 0; j < KP; ++j) kv[j] = kp[static_cast<size_t>(c * KP + j) * NPAD + col];
-    };
-    // the query means of a d-step are read just ahead of their FMAs: hoisting
-    // a whole chunk's reads would hold KP * R doubles in registers
-    auto use_chunk = [&](const double* kv, int c) {
+        for (int t = 0; t < TG; ++t)
+          bq[k % PD][t] = buffer_load_f64(krs, frag + (c0 + 16 * t) * 8, 4 * k * NPAD * 8);
+      };
 #pragma unroll
-      for (int j = 0; j < KP; ++j) {
-        const double* qrow = qs[c * KP + j];
+      for (int p = 0; p < PD; ++p) load_ab(p);
 #pragma unroll
-        for (int i = 0; i < R; i += 2) {
-          const double2 qq = *reinterpret_cast<const double2*>(qrow + i);
-          acc[i] = fma(qq.x, kv[j], acc[i]);
-          acc[i + 1] = fma(qq.y, kv[j], acc[i + 1]);
-        }
-        if constexpr (E >= 5) {
-          if (j % 2 == 1) __builtin_amdgcn_sched_barrier(0);
-        }
+      for (int k = 0; k < KS; ++k) {
+#pragma unroll
+        for (int t = 0; t < TG; ++t)
+          acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(aq[k % PD], bq[k % PD][t], acc[t], 0, 0, 0);
+        if (k + PD < KS) load_ab(k + PD);
       }
-    };
-    double ka[KP], kb[KP];
-    load_chunk(ka, 0);
-#pragma unroll CUNR
-    for (int c = 0; c < D / KP; c += 2) {
-      load_chunk(kb, c + 1);
-      use_chunk(ka, c);
-      if (c + 2 < D / KP) load_chunk(ka, c + 2);
-      use_chunk(kb, c + 1);
-    }
 #pragma unroll
-    for (int i = 0; i < R; ++i) gs[i][col] = acc[i] * scale;
+      for (int t = 0; t < TG; ++t)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) gs[hi + 4 * v][c0 + 16 * t + lo] = acc[t][v] * scale;
+    }
+  } else {
+    constexpr int KP = 8;  // d-steps of key values in flight per lane
+    static_assert(D % (2 * KP) == 0 && R % 2 == 0, "chunking");
+    double(*qs)[R] = reinterpret_cast<double(*)[R]>(lds + R * NPAD);
+    for (int i = tid; i < D * R; i += kMaskThreads) qs[i / R][i % R] = qp[(i / R) * NPAD + i % R];
+    __syncthreads();
+#pragma unroll 1
+    for (int cg = wave; cg < E; cg += kMaskWaves) {
+      const int col = 64 * cg + lane;
+      double acc[R];
+#pragma unroll
+      for (int i = 0; i < R; ++i) acc[i] = 0.0;
+      // key values of chunk c (KP d-steps) alternate between ka and kb
+      auto load_chunk = [&](double* kv, int c) {
+#pragma unroll
+        for (int j = 0; j < KP; ++j) kv[j] = buffer_load_f64(krs, col * 8, (c * KP + j) * NPAD * 8);
+      };
+      // The FMAs of each d-step are pinned before the query reads of the
+      // next: left free, the compiler hoisted every LDS read of two chunks
+      // above their FMAs and spilled them.
+      auto use_chunk = [&](const double* kv, int c) {
+#pragma unroll
+        for (int j = 0; j < KP; ++j) {
+          const double* qrow = qs[c * KP + j];
+#pragma unroll
+          for (int i = 0; i < R; i += 2) {
+            const double2 qq = *reinterpret_cast<const double2*>(qrow + i);
+            acc[i] = fma(qq.x, kv[j], acc[i]);
+            acc[i + 1] = fma(qq.y, kv[j], acc[i + 1]);
+          }
+#pragma unroll
+          for (int i = 0; i < R; ++i) asm volatile("" : "+v"(acc[i])::"memory");
+        }
+      };
+      double ka[KP], kb[KP];
+      load_chunk(ka, 0);
+#pragma unroll 1
+      for (int c = 0; c < D / KP; c += 2) {
+        load_chunk(kb, c + 1);
+        use_chunk(ka, c);
+        if (c + 2 < D / KP) load_chunk(ka, c + 2);
+        use_chunk(kb, c + 1);
+      }
+#pragma unroll
+      for (int i = 0; i < R; ++i) gs[i][col] = acc[i] * scale;
+    }
   }
   __syncthreads();
 
@@ -292,7 +356,7 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int col = 64 * e + lane;
-      const double gval = gs[i][col];
+      const double gval = col < n_b ? gs[i][col] : 0.0;
       keys[e] = col < n_b ? desc_double_asc_index_key(gval, static_cast<uint32_t>(col)) : ~0ull;
       if (scores != nullptr && col < n_b) scores[row * n_b + col] = static_cast<float>(gval);
     }

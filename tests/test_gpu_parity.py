@@ -257,8 +257,8 @@ def test_bitwise_reproducible_and_accumulate():
 # the pooled means and mask rows are padded to 64 * E columns, E in
 # {1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32}: one case per width beyond
 # the powers of two, ragged tails, every list and G compared with the oracle
-@pytest.mark.parametrize("n_b,E", [(150, 3), (300, 5), (370, 6), (600, 10), (700, 12),
-                                   (1100, 20), (1400, 24)])
+@pytest.mark.parametrize("n_b,E", [(150, 3), (300, 5), (370, 6), (480, 8), (600, 10),
+                                   (640, 10), (700, 12), (1000, 16), (1100, 20), (1400, 24)])
 def test_block_mask_at_padded_widths(n_b, E):
     w = BASE.with_(name=f"w{n_b}", H=2, d=64, block=64, frames=1, rows=1,
                    cols=64 * n_b - 21, L_a=16, n_plant=2)
