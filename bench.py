@@ -11,11 +11,12 @@ the layer (4*B*H*L_v^2*d / layer time), ``ms_per_step`` = ms per layer, a
 per-call breakdown from HIP events, the roofline of the dominant kernel
 (block-sparse attention, bf16 MFMA; against the published peak and against the
 sustained MFMA rate measured on the device), the speedup over the same kernel
-run with every list full, and the fp64 oracle timed on a bounded sample.
-``token_protection`` reports the token-granular form of the protection on
-the same inputs (protected tokens instead of protected query blocks), and
-``cache_indicator`` the cache-reuse indicator on block outputs of the same
-size (HBM-bound).
+run with every list full, and the whole fp64 oracle layer timed on the
+host.  ``token_protection`` reports the token-granular form of the
+protection on the same inputs (protected tokens instead of protected query
+blocks), ``cache_indicator`` the cache-reuse indicator on block outputs of
+the same size (HBM-bound), and ``graph`` the layer and the audio branch
+replayed from HIP graphs (the same kernels without host launch gaps).
 """
 from __future__ import annotations
 
@@ -65,6 +66,9 @@ def parse():
     p.add_argument("--no-cross-attention", action="store_true",
                    help="skip timing the cross-modal attention forwards and the saliency "
                         "from their LSEs")
+    p.add_argument("--no-graph", action="store_true",
+                   help="skip the graph-replay leg (the layer and the audio branch "
+                        "captured into HIP graphs)")
     p.add_argument("--no-audio-branch", action="store_true",
                    help="skip timing the audio branch's protected sparse attention")
     p.add_argument("--sweep", default=None,
@@ -196,12 +200,13 @@ def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
     return wall * 1e3 / steps, per_call, kv_idx.cpu().numpy(), kv_cnt.cpu().numpy()
 
 
-def time_audio_branch(plan, t, w, steps, warmup, torch, sa):
+def make_audio_branch(plan, t, w, torch, sa):
     """The audio branch's protected sparse self-attention (Eq. (8)-(11),
     m = a) at the workload's audio shape, on the audio-token saliency of the
     layer's cross scores: lagged update, protected audio tokens, the audio
     block pattern, block-sparse attention and the dense rows.  V^a is drawn
-    on the device.  Returns (ms per branch, per-call ms, computed flops)."""
+    on the device.  Returns (step, call names, kv_idx, kv_cnt, k_tok), with
+    step(e) recording event e[j] before call j when given."""
     dev = t["q_a"].device
     g = torch.Generator(device="cuda").manual_seed(1)
     v_a = torch.randn(t["q_a"].shape, device=dev, generator=g).to(t["q_a"].dtype)
@@ -240,6 +245,14 @@ def time_audio_branch(plan, t, w, steps, warmup, torch, sa):
                                         ws=ws_tok)
         rec(5)
 
+    return step, names, kv_idx, kv_cnt, k_tok
+
+
+def time_audio_branch(plan, t, w, steps, warmup, torch, sa):
+    """Times the audio branch call by call (HIP events, host launch gaps
+    included in the wall time).  Returns (ms per branch, per-call ms,
+    computed flops)."""
+    step, names, kv_idx, kv_cnt, k_tok = make_audio_branch(plan, t, w, torch, sa)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -254,6 +267,36 @@ def time_audio_branch(plan, t, w, steps, warmup, torch, sa):
     flops = (computed_flops(kv_idx.cpu().numpy(), kv_cnt.cpu().numpy(), w.L_a, w.block_a, w.d)
              + 4.0 * w.d * k_tok * w.L_a * w.B * w.H)
     return wall * 1e3 / steps, per_call, flops
+
+
+def time_graph(fn, steps, warmup, torch):
+    """fn's kernels captured once into a HIP graph (torch.cuda.CUDAGraph) and
+    replayed: (ms per replay from HIP events, ms per replay of wall time).
+    The library allocates nothing and records no memory set, so the graph
+    holds only its kernels."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(max(1, warmup)):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        fn()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) / steps, wall * 1e3 / steps
 
 
 def error_by_rank(plan, t, w, x, di, dc, k_tok, torch, sa):
@@ -641,6 +684,18 @@ def main():
             "ms": round(ms_a, 4), "per_call_ms": {k: round(v, 4) for k, v in pc_a.items()},
             "computed_tflop": round(flops_a / 1e12, 5),
             "effective_dense_tflops": round(dense_a / (ms_a * 1e-3) / 1e12, 2)}
+    if not args.no_graph:
+        # the same calls replayed from HIP graphs: no host launch gaps
+        def layer():
+            plan.run(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+        g_ms, g_wall = time_graph(layer, args.steps, args.warmup, torch)
+        res["graph"] = {"layer_ms": round(g_ms, 4), "layer_wall_ms": round(g_wall, 4),
+                        "layer_value": round(dense_flops / (g_ms * 1e-3) / 1e12, 3)}
+        if not args.no_audio_branch:
+            step_a = make_audio_branch(plan, t, w, torch, sa)[0]
+            a_ms, a_wall = time_graph(step_a, args.steps, args.warmup, torch)
+            res["graph"].update({"audio_branch_ms": round(a_ms, 4),
+                                 "audio_branch_wall_ms": round(a_wall, 4)})
     if not args.no_cache_indicator:
         ci_ms, ci_bytes = time_cache_indicator(w, args.steps, torch, sa)
         ci_gbs = ci_bytes / (ci_ms * 1e-3) / 1e9
