@@ -159,14 +159,17 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
 // wider rows use fp64 FMAs on the vector ALUs.
 __host__ __device__ constexpr bool mask_uses_mfma(int E) { return E <= 10; }
 
-// Waves per mask workgroup.  Matrix-core path: 8, which with at most 113
-// VGPRs lets two 16-row workgroups share a CU (at 5 waves and 144 VGPRs a CU
-// held one, and the n_b = 591 mask took 290 instead of 205 us; at 8 waves
-// 153 us).  Vector path: a divisor of E from 4 up, so that every wave
-// computes the scores of as many 64-column groups; 4 when E has no such
-// divisor up to 6.
+// Waves per mask workgroup.  Matrix-core path: 16 up to 384 columns (one
+// row per wave in the selection; at <= 64 VGPRs two workgroups fill a CU's
+// 32 wave slots), 8 for 512 and 640 columns, which with at most 113 VGPRs
+// lets two 16-row workgroups of 64-80 KB share a CU (at 5 waves and 144
+// VGPRs a CU held one, and the n_b = 591 mask took 290 instead of 205 us; at
+// 8 waves 153 us, at 16 waves, one workgroup per CU, 205 us).  Vector path:
+// a divisor of E from 4 up, so that every wave computes the scores of as
+// many 64-column groups; 4 when E has no such divisor up to 6.
 __host__ __device__ constexpr int mask_waves(int E) {
-  return mask_uses_mfma(E) ? 8 : (E % 4 == 0 ? 4 : (E % 5 == 0 ? 5 : (E % 6 == 0 ? 6 : 4)));
+  return mask_uses_mfma(E) ? (E <= 6 ? 16 : 8)
+                           : (E % 4 == 0 ? 4 : (E % 5 == 0 ? 5 : (E % 6 == 0 ? 6 : 4)));
 }
 
 // Query-block rows per mask workgroup: 16 on the matrix-core path (its tile
