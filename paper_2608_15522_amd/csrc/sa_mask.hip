@@ -226,7 +226,7 @@ __device__ __forceinline__ double buffer_load_f64(__amdgpu_buffer_rsrc_t r, int 
 //  * matrix-core path (R = 16): wave w takes the pairs of 16-column tiles
 //    w, w+W, ...; per 4 d-steps one A fragment (query means) and one B
 //    fragment per tile come from global memory, PD steps ahead, and each
-//    tile takes one v_mfma_f64_16x16x4f64.  Tiles past n_pad are skipped.
+//    tile takes one v_mfma_f64_16x16x4f64 (n_pad / 16 tiles in all).
 //  * vector path: the workgroup's query means are copied to LDS as [d][R];
 //    wave w takes the 64-column groups w, w+W, ..., one column per lane: the
 //    lane's key means are loaded KP d-steps ahead and each feeds R fp64 FMAs
