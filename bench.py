@@ -66,6 +66,9 @@ def parse():
     p.add_argument("--no-cross-attention", action="store_true",
                    help="skip timing the cross-modal attention forwards and the saliency "
                         "from their LSEs")
+    p.add_argument("--no-pooled", action="store_true",
+                   help="skip the layer with the block means pooled inside the saliency "
+                        "streams")
     p.add_argument("--no-graph", action="store_true",
                    help="skip the graph-replay leg (the layer and the audio branch "
                         "captured into HIP graphs)")
@@ -146,6 +149,49 @@ def time_layer(plan, t, steps, warmup, torch):
     med = {n: sorted(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps))[steps // 2]
            for j, n in enumerate(names)}
     return wall * 1e3 / steps, per_call, med
+
+
+def time_pooled_layer(plan, t, steps, warmup, torch):
+    """The layer with the mask's block means pooled inside the saliency
+    streams (sa_cross_scores_pooled, select, sa_build_block_mask_pooled,
+    attention) against the plain layer, the two alternating step by step so
+    that clock drift under the power limit falls on both alike.  Returns
+    (per-call median ms of the pooled layer, of the plain layer)."""
+    args = (t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+    for _ in range(warmup):
+        plan.run_pooled(*args)
+        plan.run(*args)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(steps)]
+    for i in range(steps):
+        e = ev[i]
+        e[0].record()
+        plan.cross_scores_pooled(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        e[1].record()
+        plan.select_protected()
+        e[2].record()
+        plan.build_block_mask_pooled()
+        e[3].record()
+        plan.sparse_attention(t["q_v"], t["k_v"], t["v_v"])
+        e[4].record()
+        plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        e[5].record()
+        plan.select_protected()
+        e[6].record()
+        plan.build_block_mask(t["q_v"], t["k_v"])
+        e[7].record()
+        plan.sparse_attention(t["q_v"], t["k_v"], t["v_v"])
+        e[8].record()
+    torch.cuda.synchronize()
+
+    def med(j0, names):
+        return {n: sorted(ev[i][j0 + j].elapsed_time(ev[i][j0 + j + 1])
+                          for i in range(steps))[steps // 2] for j, n in enumerate(names)}
+    pooled = med(0, ["sa_cross_scores_pooled", "sa_select_protected",
+                     "sa_build_block_mask_pooled", "sa_sparse_attention"])
+    plain = med(4, ["sa_cross_scores", "sa_select_protected", "sa_build_block_mask",
+                    "sa_sparse_attention"])
+    return pooled, plain
 
 
 def time_token_layer(plan, t, w, k_tok, alpha, steps, warmup, torch, sa):
@@ -367,7 +413,9 @@ def time_cross_attention(plan, t, w, steps, warmup, torch, sa):
         return torch.empty(max(1, sa.sa_workspace_size(sa.SA_CALL_CROSS_ATTENTION, B, H, Lq, Lk,
                                                        d, 0)), dtype=torch.uint8, device=dev)
     ws_a, ws_v = ws(L_a, L_v), ws(L_v, L_a)
-    names = ["a2v_forward", "v2a_forward", "sa_cross_scores_from_lse", "sa_cross_scores"]
+    names = ["a2v_forward", "v2a_forward", "sa_cross_scores_from_lse", "sa_cross_scores",
+             "sa_build_block_mask", "sa_cross_scores_pooled_from_lse",
+             "sa_build_block_mask_pooled"]
 
     def step(e=None):
         rec = (lambda j: e[j].record()) if e else (lambda j: None)
@@ -384,11 +432,18 @@ def time_cross_attention(plan, t, w, steps, warmup, torch, sa):
         rec(3)
         plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
         rec(4)
+        plan.build_block_mask(t["q_v"], t["k_v"])
+        rec(5)
+        plan.cross_scores_pooled(t["q_a"], t["k_v"], t["q_v"], t["k_a"], lse_a=lse_a,
+                                 lse_v=lse_v)
+        rec(6)
+        plan.build_block_mask_pooled()
+        rec(7)
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(steps)]
     for i in range(steps):
         step(ev[i])
     torch.cuda.synchronize()
@@ -401,7 +456,14 @@ def time_cross_attention(plan, t, w, steps, warmup, torch, sa):
             "a2v_forward_tflops": round(flops / (ms["a2v_forward"] * 1e-3) / 1e12, 1),
             "v2a_forward_tflops": round(flops / (ms["v2a_forward"] * 1e-3) / 1e12, 1),
             "forwards_plus_saliency_ms": round(fwd_ms + ms["sa_cross_scores_from_lse"], 4),
-            "forwards_plus_standalone_saliency_ms": round(fwd_ms + ms["sa_cross_scores"], 4)}
+            "forwards_plus_standalone_saliency_ms": round(fwd_ms + ms["sa_cross_scores"], 4),
+            # steps 1-2 on top of the forwards: saliency from their LSEs and the
+            # block mask, with the mask call pooling Q^v, K^v itself, or with the
+            # means pooled inside the saliency streams
+            "saliency_plus_mask_ms": round(ms["sa_cross_scores_from_lse"]
+                                           + ms["sa_build_block_mask"], 4),
+            "saliency_plus_mask_pooled_ms": round(ms["sa_cross_scores_pooled_from_lse"]
+                                                  + ms["sa_build_block_mask_pooled"], 4)}
 
 
 def time_cache_indicator(w, steps, torch, sa):
@@ -652,6 +714,19 @@ def main():
             "random_operands_tflops": round(rnd_tf, 1), "random_operands_ghz": round(rnd_ghz, 2),
             "zero_operands_tflops": round(zero_tf, 1), "zero_operands_ghz": round(zero_ghz, 2),
             "frac_of_random_operands": round(achieved / rnd_tf, 4)}
+    if not args.no_pooled:
+        pc_p, pc_0 = time_pooled_layer(plan, t, args.steps, args.warmup, torch)
+        print(f"bench: pooled layer {pc_p}, plain layer {pc_0}", file=sys.stderr, flush=True)
+        res["pooled_layer"] = {
+            "timing": "medians, pooled and plain layers alternating step by step",
+            "per_call_median_ms": {k: round(v, 4) for k, v in pc_p.items()},
+            "plain_per_call_median_ms": {k: round(v, 4) for k, v in pc_0.items()},
+            "layer_ms": round(sum(pc_p.values()), 4),
+            "plain_layer_ms": round(sum(pc_0.values()), 4),
+            "steps_1_2_ms": round(pc_p["sa_cross_scores_pooled"]
+                                  + pc_p["sa_build_block_mask_pooled"], 4),
+            "plain_steps_1_2_ms": round(pc_0["sa_cross_scores"]
+                                        + pc_0["sa_build_block_mask"], 4)}
     if args.token_rho > 0:
         k_tok = synth.budget(args.token_rho, w.L_v)
         ms_tok, pc_tok, kvi_tok, kvc_tok = time_token_layer(

@@ -209,6 +209,64 @@ int sa_build_block_mask(const void* q_v, const void* k_v, int B, int H,
                         void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Pooling fused into the saliency streams.  The mask's block means (Sec. 4.2,
+ * Eq. (6)) are taken from the same Q^v and K^v that the saliency of Sec. 4.1
+ * (Eq. (1)-(2) and the reverse direction) reads, so one pass over each serves
+ * both: sa_cross_scores_pooled writes them, sa_build_block_mask_pooled ranks
+ * them.  The pair gives the same lists as sa_cross_scores (or
+ * sa_cross_scores_from_lse) followed by sa_build_block_mask: the means are
+ * exact fp64 sums of the bf16 (or fp32) inputs divided once, as there.
+ *
+ * Layout of the means: qbar and kbar are each [B,H,d,n_pad] fp64 (block index
+ * innermost), n_pad = sa_pool_columns(n_b); columns n_b .. n_pad-1 are never
+ * written or read as scores.
+ */
+
+/* Columns n_pad of the pooled means for n_b blocks (0 if n_b is outside
+ * [1, 2048]). */
+int sa_pool_columns(int n_b);
+
+/*
+ * sa_cross_scores_pooled -- the saliency of sa_cross_scores (lse_a and lse_v
+ * NULL) or of sa_cross_scores_from_lse (both given: the row LSEs of the two
+ * sa_cross_attention forwards), plus the block means of Q^v and K^v.
+ *
+ * Both directions are computed (q_v, k_a, sal_a_tok are required).  With
+ * bf16 inputs the means come from the streams of the column-mass passes:
+ * K^v from the a->v pass (its first slab of audio queries), Q^v from the
+ * rows each v->a workgroup holds.  fp32 inputs (standalone form only) pool
+ * in a separate pass.  Other arguments and results as in sa_cross_scores.
+ *
+ *   lse_a, lse_v  [B,H,L_a], [B,H,L_v] f32, both NULL or both non-NULL
+ *                 (non-NULL: SA_BF16 only)
+ *   qbar, kbar    out, [B,H,d,sa_pool_columns(n_b)] fp64 each, 8-byte
+ *                 aligned, not overlapping
+ *   ws            workspace of at least sa_workspace_size(SA_CALL_CROSS_SCORES)
+ */
+int sa_cross_scores_pooled(const void* q_a, const void* k_v, const void* q_v,
+                           const void* k_a, const float* lse_a,
+                           const float* lse_v, int B, int H, int L_v, int L_a,
+                           int d, int dtype, float scale, int block,
+                           float* sal_v_tok, float* sal_v_blk,
+                           float* sal_a_tok, int accumulate, double* qbar,
+                           double* kbar, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/*
+ * sa_build_block_mask_pooled -- sa_build_block_mask from the block means that
+ * sa_cross_scores_pooled wrote (Sec. 4.2, Eq. (6) and (9)): G, the ranking,
+ * the protection and the outputs are those of sa_build_block_mask.  d, block
+ * and L_v must be those of the pooling call.  No workspace.
+ *
+ *   qbar, kbar [B,H,d,sa_pool_columns(n_b)] fp64 in, 8-byte aligned
+ */
+int sa_build_block_mask_pooled(const double* qbar, const double* kbar, int B,
+                               int H, int L_v, int d, float scale, int block,
+                               int k_keep, const uint8_t* prot_flag,
+                               int32_t* kv_idx, int32_t* kv_cnt,
+                               uint8_t* mask, float* scores, void* stream);
+
+/*
  * sa_sparse_attention -- protected block-sparse attention (Sec. 4.2,
  * Eq. (10) in its row form Eq. (11)).
  *

@@ -47,6 +47,11 @@ SIGNATURES = {
                                 _SZ, _VP]),
     "sa_cross_scores_from_lse": (_I, [_VP, _VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _I,
                                       _F, _I, _VP, _VP, _VP, _I, _VP, _SZ, _VP]),
+    "sa_pool_columns": (_I, [_I]),
+    "sa_cross_scores_pooled": (_I, [_VP, _VP, _VP, _VP, _VP, _VP, _I, _I, _I, _I, _I, _I,
+                                    _F, _I, _VP, _VP, _VP, _I, _VP, _VP, _VP, _SZ, _VP]),
+    "sa_build_block_mask_pooled": (_I, [_VP, _VP, _I, _I, _I, _I, _F, _I, _I, _VP, _VP, _VP,
+                                        _VP, _VP, _VP]),
     "sa_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "sa_last_error": (ctypes.c_char_p, []),
     "sa_version": (_I, []),
@@ -315,6 +320,81 @@ def sa_cross_scores_from_lse(q_a, k_v, q_v, k_a, lse_a, lse_v, scale, block, *,
         L_a, d, _dtype_code(q_a), float(scale), block, _ptr(sal_v_tok), _ptr(sal_v_blk),
         _ptr(sal_a_tok), int(bool(accumulate)), _ptr(ws), _nbytes(ws), _stream()))
     return sal_v_tok, sal_v_blk, sal_a_tok
+
+
+def sa_pool_columns(n_b: int) -> int:
+    """Columns n_pad of the pooled block means (0 for an unsupported n_b)."""
+    return int(lib().sa_pool_columns(int(n_b)))
+
+
+def sa_cross_scores_pooled(q_a, k_v, q_v, k_a, scale, block, *, lse_a=None, lse_v=None,
+                           sal_v_tok=None, sal_v_blk=None, sal_a_tok=None, qbar=None,
+                           kbar=None, accumulate=False, want_tok=True, ws=None):
+    """The saliency of both directions (standalone, or from the forwards' row
+    LSEs when lse_a and lse_v are given) plus the block means of Q^v and K^v;
+    returns (sal_v_tok, sal_v_blk, sal_a_tok, qbar, kbar), the means as
+    [B,H,d,n_pad] float64."""
+    B, H, L_a, d = q_a.shape
+    L_v = k_v.shape[2]
+    n_b = -(-L_v // block)
+    n_pad = sa_pool_columns(n_b)
+    dev = q_a.device
+    _expect(k_v, "k_v", (B, H, L_v, d), q_a.dtype)
+    _expect(q_v, "q_v", (B, H, L_v, d), q_a.dtype)
+    _expect(k_a, "k_a", (B, H, L_a, d), q_a.dtype)
+    _expect(lse_a, "lse_a", (B, H, L_a), torch.float32)
+    _expect(lse_v, "lse_v", (B, H, L_v), torch.float32)
+    _expect(sal_v_tok, "sal_v_tok", (B, L_v), torch.float32)
+    _expect(sal_v_blk, "sal_v_blk", (B, n_b), torch.float32)
+    _expect(sal_a_tok, "sal_a_tok", (B, L_a), torch.float32)
+    _expect(qbar, "qbar", (B, H, d, n_pad), torch.float64)
+    _expect(kbar, "kbar", (B, H, d, n_pad), torch.float64)
+    if sal_v_blk is None:
+        sal_v_blk = torch.empty(B, n_b, dtype=torch.float32, device=dev)
+    if sal_v_tok is None and want_tok:
+        sal_v_tok = torch.empty(B, L_v, dtype=torch.float32, device=dev)
+    if sal_a_tok is None:
+        sal_a_tok = torch.empty(B, L_a, dtype=torch.float32, device=dev)
+    if qbar is None:
+        qbar = torch.empty(B, H, d, n_pad, dtype=torch.float64, device=dev)
+    if kbar is None:
+        kbar = torch.empty(B, H, d, n_pad, dtype=torch.float64, device=dev)
+    ws = _workspace(SA_CALL_CROSS_SCORES, B, H, L_v, L_a, d, block, dev, ws)
+    _check(lib().sa_cross_scores_pooled(
+        _ptr(q_a), _ptr(k_v), _ptr(q_v), _ptr(k_a), _ptr(lse_a), _ptr(lse_v), B, H, L_v,
+        L_a, d, _dtype_code(q_a), float(scale), block, _ptr(sal_v_tok), _ptr(sal_v_blk),
+        _ptr(sal_a_tok), int(bool(accumulate)), _ptr(qbar), _ptr(kbar), _ptr(ws),
+        _nbytes(ws), _stream()))
+    return sal_v_tok, sal_v_blk, sal_a_tok, qbar, kbar
+
+
+def sa_build_block_mask_pooled(qbar, kbar, L_v, scale, block, k_keep, prot_flag=None, *,
+                               kv_idx=None, kv_cnt=None, want_mask=False,
+                               want_scores=False, mask=None, scores=None):
+    """sa_build_block_mask from the means of sa_cross_scores_pooled; returns
+    (kv_idx, kv_cnt, mask, scores)."""
+    B, H, d, n_pad = qbar.shape
+    n_b = -(-L_v // block)
+    dev = qbar.device
+    _expect(qbar, "qbar", (B, H, d, sa_pool_columns(n_b)), torch.float64)
+    _expect(kbar, "kbar", (B, H, d, n_pad), torch.float64)
+    _expect(prot_flag, "prot_flag", (B, n_b), torch.uint8)
+    _expect(kv_idx, "kv_idx", (B, H, n_b, n_b), torch.int32)
+    _expect(kv_cnt, "kv_cnt", (B, H, n_b), torch.int32)
+    _expect(mask, "mask", (B, H, n_b, n_b), torch.uint8)
+    _expect(scores, "scores", (B, H, n_b, n_b), torch.float32)
+    if kv_idx is None:
+        kv_idx = torch.empty(B, H, n_b, n_b, dtype=torch.int32, device=dev)
+    if kv_cnt is None:
+        kv_cnt = torch.empty(B, H, n_b, dtype=torch.int32, device=dev)
+    if mask is None and want_mask:
+        mask = torch.empty(B, H, n_b, n_b, dtype=torch.uint8, device=dev)
+    if scores is None and want_scores:
+        scores = torch.empty(B, H, n_b, n_b, dtype=torch.float32, device=dev)
+    _check(lib().sa_build_block_mask_pooled(
+        _ptr(qbar), _ptr(kbar), B, H, L_v, d, float(scale), block, int(k_keep),
+        _ptr(prot_flag), _ptr(kv_idx), _ptr(kv_cnt), _ptr(mask), _ptr(scores), _stream()))
+    return kv_idx, kv_cnt, mask, scores
 
 
 def sa_saliency_ema(sal_bar, sal, alpha):

@@ -245,7 +245,8 @@ int sa_cross_scores(const void* q_a, const void* k_v, const void* q_v, const voi
     sa::launch_cross_scores_bf16(
         static_cast<const uint16_t*>(q_a), static_cast<const uint16_t*>(k_v),
         static_cast<const uint16_t*>(q_v), static_cast<const uint16_t*>(k_a), B, H, L_v,
-        L_a, d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, w, s);
+        L_a, d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, nullptr, nullptr,
+        w, s);
   else
     sa::launch_cross_scores_f32(
         static_cast<const float*>(q_a), static_cast<const float*>(k_v),
@@ -283,8 +284,68 @@ int sa_cross_scores_from_lse(const void* q_a, const void* k_v, const void* q_v,
   sa::launch_cross_scores_from_lse_bf16(
       static_cast<const uint16_t*>(q_a), static_cast<const uint16_t*>(k_v),
       static_cast<const uint16_t*>(q_v), static_cast<const uint16_t*>(k_a), lse_a, lse_v, B, H,
-      L_v, L_a, d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate,
+      L_v, L_a, d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, nullptr, nullptr,
       static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_pool_columns(int n_b) {
+  if (n_b < 1 || n_b > sa::kMaxBlocks) return 0;
+  return sa::mask_n_pad(n_b);
+}
+
+int sa_cross_scores_pooled(const void* q_a, const void* k_v, const void* q_v, const void* k_a,
+                           const float* lse_a, const float* lse_v, int B, int H, int L_v,
+                           int L_a, int d, int dtype, float scale, int block, float* sal_v_tok,
+                           float* sal_v_blk, float* sal_a_tok, int accumulate, double* qbar,
+                           double* kbar, void* ws, size_t ws_bytes, void* stream) {
+  const char* fn = "sa_cross_scores_pooled";
+  SA_TRY(check_common(fn, B, H, L_v, d, dtype, scale, block));
+  if (L_a < 1) return fail(SA_ERR_INVALID_ARG, "%s: L_a=%d must be >= 1", fn, L_a);
+  if (accumulate != 0 && accumulate != 1)
+    return fail(SA_ERR_INVALID_ARG, "%s: accumulate=%d must be 0 or 1", fn, accumulate);
+  const bool from_lse = lse_a != nullptr;
+  if ((lse_v != nullptr) != from_lse)
+    return fail(SA_ERR_INVALID_ARG, "%s: lse_a and lse_v must be both NULL or both non-NULL",
+                fn);
+  if (from_lse && dtype != SA_BF16)
+    return fail(SA_ERR_UNSUPPORTED, "%s: the LSE form takes SA_BF16 inputs only", fn);
+  SA_TRY(check_tensor(fn, "q_a", q_a, true, 16));
+  SA_TRY(check_tensor(fn, "k_v", k_v, true, 16));
+  SA_TRY(check_tensor(fn, "q_v", q_v, true, 16));
+  SA_TRY(check_tensor(fn, "k_a", k_a, true, 16));
+  SA_TRY(check_tensor(fn, "lse_a", lse_a, false, 4));
+  SA_TRY(check_tensor(fn, "lse_v", lse_v, false, 4));
+  SA_TRY(check_tensor(fn, "sal_v_tok", sal_v_tok, false, 4));
+  SA_TRY(check_tensor(fn, "sal_v_blk", sal_v_blk, true, 4));
+  SA_TRY(check_tensor(fn, "sal_a_tok", sal_a_tok, true, 4));
+  SA_TRY(check_tensor(fn, "qbar", qbar, true, 8));
+  SA_TRY(check_tensor(fn, "kbar", kbar, true, 8));
+  const size_t nmean = static_cast<size_t>(B) * H * d * sa::mask_n_pad(sa::ceil_div(L_v, block));
+  if (qbar < kbar + nmean && kbar < qbar + nmean)
+    return fail(SA_ERR_INVALID_ARG, "%s: qbar and kbar overlap (each holds %zu doubles)", fn,
+                nmean);
+  SA_TRY(check_ws(fn, ws, ws_bytes, sa::cross_ws_layout(B, H, L_v, L_a).total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const uint16_t* qa16 = static_cast<const uint16_t*>(q_a);
+  const uint16_t* kv16 = static_cast<const uint16_t*>(k_v);
+  const uint16_t* qv16 = static_cast<const uint16_t*>(q_v);
+  const uint16_t* ka16 = static_cast<const uint16_t*>(k_a);
+  if (from_lse) {
+    sa::launch_cross_scores_from_lse_bf16(qa16, kv16, qv16, ka16, lse_a, lse_v, B, H, L_v, L_a,
+                                          d, scale, block, sal_v_tok, sal_v_blk, sal_a_tok,
+                                          accumulate, qbar, kbar, w, s);
+  } else if (dtype == SA_BF16) {
+    sa::launch_cross_scores_bf16(qa16, kv16, qv16, ka16, B, H, L_v, L_a, d, scale, block,
+                                 sal_v_tok, sal_v_blk, sal_a_tok, accumulate, qbar, kbar, w, s);
+  } else {  // the fp32 correctness path pools in a pass of its own
+    sa::launch_cross_scores_f32(
+        static_cast<const float*>(q_a), static_cast<const float*>(k_v),
+        static_cast<const float*>(q_v), static_cast<const float*>(k_a), B, H, L_v, L_a, d,
+        scale, block, sal_v_tok, sal_v_blk, sal_a_tok, accumulate, w, s);
+    sa::launch_block_pool(q_v, k_v, B, H, L_v, d, dtype, block, qbar, kbar, s);
+  }
   return check_launch(fn);
 }
 
@@ -349,6 +410,27 @@ int sa_build_block_mask(const void* q_v, const void* k_v, int B, int H, int L_v,
   sa::launch_build_block_mask(q_v, k_v, B, H, L_v, d, dtype, scale, block, k_keep,
                               prot_flag, kv_idx, kv_cnt, mask, scores,
                               static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+  return check_launch(fn);
+}
+
+int sa_build_block_mask_pooled(const double* qbar, const double* kbar, int B, int H, int L_v,
+                               int d, float scale, int block, int k_keep,
+                               const uint8_t* prot_flag, int32_t* kv_idx, int32_t* kv_cnt,
+                               uint8_t* mask, float* scores, void* stream) {
+  const char* fn = "sa_build_block_mask_pooled";
+  SA_TRY(check_common(fn, B, H, L_v, d, SA_BF16, scale, block));
+  const int n_b = sa::ceil_div(L_v, block);
+  if (k_keep < 1 || k_keep > n_b)
+    return fail(SA_ERR_INVALID_ARG, "%s: k_keep=%d outside [1, n_b=%d]", fn, k_keep, n_b);
+  SA_TRY(check_tensor(fn, "qbar", qbar, true, 8));
+  SA_TRY(check_tensor(fn, "kbar", kbar, true, 8));
+  SA_TRY(check_tensor(fn, "prot_flag", prot_flag, false, 1));
+  SA_TRY(check_tensor(fn, "kv_idx", kv_idx, true, 4));
+  SA_TRY(check_tensor(fn, "kv_cnt", kv_cnt, true, 4));
+  SA_TRY(check_tensor(fn, "mask", mask, false, 1));
+  SA_TRY(check_tensor(fn, "scores", scores, false, 4));
+  sa::launch_mask_from_means(qbar, kbar, B, H, L_v, d, scale, block, k_keep, prot_flag, kv_idx,
+                             kv_cnt, mask, scores, static_cast<hipStream_t>(stream));
   return check_launch(fn);
 }
 

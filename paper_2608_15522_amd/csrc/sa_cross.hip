@@ -308,6 +308,215 @@ struct ColAcc {
   __device__ __forceinline__ void fin(const f32x16 (&)[2], int u, bool) { red[32 * u] += cs; }
 };
 
+// ---- block means fused into the streams (Sec. 4.2, Eq. (6)) ------------------
+// The mean of Q^v and of K^v over each block of `block` tokens (the last block
+// over its true length), written as [d][n_pad] per (b,h) like the mask call's
+// own pooling.  Sums of bf16 values are exact in fp64, so the means equal
+// that pooling bit for bit whatever the order of the additions.
+
+// 8 bf16 of a 16-byte chunk added to acc in fp64.
+__device__ __forceinline__ void add_bf16x8(u32x4 v, double (&acc)[8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc[2 * i] += static_cast<double>(__uint_as_float(v[i] << 16));
+    acc[2 * i + 1] += static_cast<double>(__uint_as_float(v[i] & 0xffff0000u));
+  }
+}
+
+// 4 bf16 (8 bytes) added to acc in fp64.
+__device__ __forceinline__ void add_bf16x4(u32x2 v, double (&acc)[4]) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    acc[2 * i] += static_cast<double>(__uint_as_float(v[i] << 16));
+    acc[2 * i + 1] += static_cast<double>(__uint_as_float(v[i] & 0xffff0000u));
+  }
+}
+
+// x summed over the 16 lanes of its DPP row, the same total in every lane:
+// lane pairs (quad_perm 1,0,3,2), then quads (2,3,0,1), then the two halves
+// of each 8 lanes (half-row mirror) and of the row (row mirror).  Each step
+// moves the two dwords of x with DPP and adds in fp64.
+__device__ __forceinline__ double dpp_row_sum(double x) {
+  auto step = [](double v, int ctrl) {
+    const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    const int lo = static_cast<int>(u & 0xffffffffu), hi = static_cast<int>(u >> 32);
+    int plo, phi;
+    switch (ctrl) {  // the DPP control must be a constant
+      case 0:
+        plo = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false);
+        phi = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false);
+        break;
+      case 1:
+        plo = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false);
+        phi = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false);
+        break;
+      case 2:
+        plo = __builtin_amdgcn_mov_dpp(lo, 0x141, 0xF, 0xF, false);
+        phi = __builtin_amdgcn_mov_dpp(hi, 0x141, 0xF, 0xF, false);
+        break;
+      default:
+        plo = __builtin_amdgcn_mov_dpp(lo, 0x140, 0xF, 0xF, false);
+        phi = __builtin_amdgcn_mov_dpp(hi, 0x140, 0xF, 0xF, false);
+        break;
+    }
+    const uint64_t w = (static_cast<uint64_t>(static_cast<uint32_t>(phi)) << 32) |
+                       static_cast<uint32_t>(plo);
+    return v + __longlong_as_double(static_cast<long long>(w));
+  };
+  x = step(x, 0);
+  x = step(x, 1);
+  x = step(x, 2);
+  return step(x, 3);
+}
+
+// Keys of a column-mass stream (K2), pooled from the LDS ring.  Lane l of
+// wave w takes d quarter q = 4w + l/16 (d = 4q .. 4q+3) of key rows l % 16 and
+// l % 16 + 16 of every 32-key unit, read while the unit's MFMAs run; at the end
+// of a block the 16 lanes that share q (one DPP row) add their sums
+// (dpp_row_sum), and the lane of row 0 writes the 4 means.  Waves past D/16 (d = 64) take no part.
+template <int D>
+struct KeyPool {
+  static constexpr int TB = KeyRing<D>::TB;
+  double acc[4];
+  u32x2 raw[2];
+  const char* ring;    // LDS ring, stage 0
+  int off;             // lane offset of its quarter of row l % 16 in a unit
+  int key_begin, L, block, nunits, n_pad;
+  bool on;             // wave-uniform: this wave pools
+  double* dst;         // kbar + pair * D * n_pad
+
+  __device__ __forceinline__ void init(const char* ring_lds, int wave, int lane, int key_begin_,
+                                       int L_, int block_, int T, int n_pad_, double* dst_) {
+    const int r = lane & 15;
+    const int q = 4 * wave + (lane >> 4);  // = threadIdx.x / 16
+    on = 4 * wave < D / 4;
+    const int cc = q >> 1;  // 16-byte chunk; the plane swizzle of rows r, r + 16 and
+                            // 32*kb + r is that of row r
+    off = (cc >> 2) * 4096 + r * 64 + 16 * ((cc & 3) ^ plane_swz(r)) + 8 * (q & 1);
+    ring = ring_lds;
+    key_begin = key_begin_;
+    L = L_;
+    block = block_;
+    nunits = 2 * T;
+    n_pad = n_pad_;
+    dst = dst_;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = 0.0;
+  }
+  // unit p = keys key_begin + 32p ..; tile p/2 sits in stage (p/2) % kRing
+  __device__ __forceinline__ void load(int p) {
+    if (on && p < nunits) {
+      const char* base = ring + ((p >> 1) % kRing) * TB + (p & 1) * 2048 + off;
+      raw[0] = *reinterpret_cast<const u32x2*>(base);
+      raw[1] = *reinterpret_cast<const u32x2*>(base + 16 * 64);
+    }
+  }
+  // Dword part (0..3) of the unit's two rows: 2 elements.
+  __device__ __forceinline__ void add(int p, int part) {
+    if (on && p < nunits) {
+      const int j = part >> 1, i = part & 1;
+      uint32_t v = raw[j][i];
+      // rows past L repeat row L-1 in the ring: they add nothing
+      if (key_begin + 32 * p + 32 > L && key_begin + 32 * p + (threadIdx.x & 15) + 16 * j >= L)
+        v = 0u;
+      acc[2 * i] += static_cast<double>(__uint_as_float(v << 16));
+      acc[2 * i + 1] += static_cast<double>(__uint_as_float(v & 0xffff0000u));
+    }
+  }
+  // After unit p: at the end of a block, sum over the 32 rows and write.
+  __device__ __forceinline__ void close(int p) {
+    const int upb = block >> 5;  // units per block
+    if (!on || p >= nunits || (p % upb != upb - 1 && p != nunits - 1)) return;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = dpp_row_sum(acc[e]);
+    const int c = (key_begin + 32 * p) / block;
+    const int len = min(block, L - c * block);
+    if ((threadIdx.x & 15) == 0) {
+      const int q = threadIdx.x >> 4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        dst[static_cast<size_t>(4 * q + e) * n_pad + c] = acc[e] / static_cast<double>(len);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = 0.0;
+  }
+};
+
+// ColAcc with the keys' block means: unit p = u + 1 (whose MFMAs run beside
+// the slots of unit u) is read a few slots in and added two elements at a
+// time beside four of the later MFMAs; unit 0 is pooled in first().
+template <int D>
+struct ColPoolAcc : ColAcc<D> {
+  KeyPool<D> pool;
+  static constexpr int NS = D / 8;
+  __device__ __forceinline__ void first(const f32x16 (&)[2]) {
+    pool.load(0);
+#pragma unroll
+    for (int part = 0; part < 4; ++part) pool.add(0, part);
+    pool.close(0);
+  }
+  __device__ __forceinline__ void slot(const f32x16 (&x)[2], int s, int u, bool last) {
+    constexpr int GAP = NS / 8;  // slots between two parts
+    if (s == NS / 4 - GAP) pool.load(u + 1);
+    // the four dword parts beside four of the later MFMAs
+    if (s >= NS / 4 && s < NS / 4 + 4 * GAP && (s - NS / 4) % GAP == 0)
+      pool.add(u + 1, (s - NS / 4) / GAP);
+    ColAcc<D>::slot(x, s, u, last);
+  }
+  __device__ __forceinline__ void fin(const f32x16 (&x)[2], int u, bool last) {
+    ColAcc<D>::fin(x, u, last);
+    pool.close(u + 1);
+  }
+};
+
+// Query rows of a v->a workgroup (K3), pooled from a second load of the rows
+// it has just loaded for its MFMAs (L2 hits).  Thread t takes block
+// t / block of the kV2aChunk rows from row0, 16-byte chunk cc and every
+// (block / CPR)-th row of that block (CPR rows); the partial sums go through
+// `part` (32 KB of LDS, [thread][element]) and are added in a fixed order.
+// Ends with a barrier, after which `part` may be reused.
+template <int D>
+__device__ __forceinline__ void pool_query_chunk(const uint16_t* __restrict__ src, int row0,
+                                                 int L, int block, int n_pad,
+                                                 double* __restrict__ dst, double* part) {
+  constexpr int CPR = D / 8;
+  const int t = threadIdx.x;
+  const int bl = t / block, w = t % block;
+  const int cc = w % CPR, rg = w / CPR;
+  const int RG = block / CPR;  // row groups of a block
+  const int rb = row0 + bl * block;
+  double acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+#pragma unroll
+  for (int i0 = 0; i0 < CPR; i0 += 8) {
+    u32x4 raw[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = rb + rg + RG * (i0 + i);
+      raw[i] = r < L ? ldg16(src + static_cast<size_t>(r) * D + 8 * cc)
+                     : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) add_bf16x8(raw[i], acc);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[8 * t + e] = acc[e];
+  __syncthreads();
+  const int nbl = kV2aChunk / block;
+  for (int o = t; o < nbl * D; o += kXNT) {
+    const int b2 = o / D, dd = o % D;
+    const int rs = row0 + b2 * block;
+    if (rs >= L) continue;
+    const int len = min(block, L - rs);
+    const int base = b2 * block + dd / 8;  // thread of row group 0, chunk dd / 8
+    double sum = 0.0;
+    for (int g = 0; g < RG; ++g) sum += part[8 * (base + g * CPR) + (dd & 7)];
+    dst[static_cast<size_t>(dd) * n_pad + rs / block] = sum / static_cast<double>(len);
+  }
+  __syncthreads();
+}
+
 // ---- K1 ---------------------------------------------------------------------
 template <int D>
 __global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -383,12 +592,15 @@ lse_combine_kernel(const float2* __restrict__ part, float* __restrict__ lse2, in
 // owns a key column) and adds exp2(S*c - lse) into per-lane LDS slots; the 16
 // slots of a key (8 waves x 2 lane halves) are then summed in a fixed order.
 // Keys past L_v only reach their own columns, which are not written.
-template <int D>
+// POOL: the stream of the first slab also writes the block means of K^v
+// (KeyPool) to kbar ([B,H,d,n_pad]).
+template <int D, bool POOL>
 __global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
                    const uint16_t* __restrict__ k_v,
                    const float* __restrict__ lse2, float* __restrict__ colmass,
-                   int H, int L_v, int L_a, float c) {
+                   int H, int L_v, int L_a, float c, double* __restrict__ kbar, int block,
+                   int n_pad) {
   constexpr int RS = kColKeys + 32;  // slot row stride (the two lane halves use different banks)
   __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
   __shared__ float red[2 * kXW][RS];
@@ -422,7 +634,15 @@ a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
         const int jj = j0 + 32 * hh + crow(i, g);
         acc.lr[hh][i] = jj < L_a ? lh[jj] : INFINITY;
       }
-    stream_keys<D, false>(ring, ring_lds, kh, key_begin, L_v, T, qf, acc);
+    if (POOL && slab == 0) {
+      ColPoolAcc<D> pacc;
+      static_cast<ColAcc<D>&>(pacc) = acc;
+      pacc.pool.init(ring_lds, wave, lane, key_begin, L_v, block, T, n_pad,
+                     kbar + pair * D * n_pad);
+      stream_keys<D, false>(ring, ring_lds, kh, key_begin, L_v, T, qf, pacc);
+    } else {
+      stream_keys<D, false>(ring, ring_lds, kh, key_begin, L_v, T, qf, acc);
+    }
   }
   for (int k = threadIdx.x; k < kColKeys; k += kXNT) {
     float sum = 0.f;
@@ -440,11 +660,14 @@ a2v_colmass_kernel(const uint16_t* __restrict__ q_a,
 // mass of each key over the 512 queries (per-lane LDS slots, fixed order).
 // FROM_LSE: pass 1 is replaced by the natural-log LSE of each video query
 // that a v->a cross-attention forward produced (lse_v [P][L_v]).
+// qbar != NULL: the workgroup first writes the block means of its 512 video
+// queries (pool_query_chunk) to qbar ([B,H,d,n_pad]).
 template <int D, bool FROM_LSE>
 __global__ void __launch_bounds__(kXNT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
                    const uint16_t* __restrict__ k_a, float* __restrict__ part,
-                   int L_v, int L_a, int nchunk, float c, const float* __restrict__ lse_v) {
+                   int L_v, int L_a, int nchunk, float c, const float* __restrict__ lse_v,
+                   double* __restrict__ qbar, int block, int n_pad) {
   constexpr int RS = kAWin + 32;
   __shared__ __attribute__((aligned(1024))) char ring_lds[kRing * KeyRing<D>::TB];
   __shared__ float red[2 * kXW][RS];
@@ -461,6 +684,10 @@ v2a_colmass_kernel(const uint16_t* __restrict__ q_v,
   load_qfrag<D>(qh, i0 + 32 + n, L_v, g, qf[1]);
   KeyRing<D> ring;
   ring.init(ring_lds, wave, lane);
+  if (qbar != nullptr)  // the ring is free until the first stream
+    pool_query_chunk<D>(qh, chunk * kV2aChunk, L_v, block, n_pad,
+                        qbar + static_cast<size_t>(pair) * D * n_pad,
+                        reinterpret_cast<double*>(ring_lds));
 
   if constexpr (FROM_LSE) {
 #pragma unroll
@@ -631,11 +858,26 @@ colmass_f32_kernel(const float* __restrict__ qm, const float* __restrict__ km,
   out[t] = acc;
 }
 
+// K2, with the block means of K^v written to kbar when it is not NULL.
+template <int D>
+void launch_a2v_colmass(const uint16_t* q_a, const uint16_t* k_v, const float* lse2,
+                        float* colmass, int B, int H, int L_v, int L_a, float c, double* kbar,
+                        int block, hipStream_t s) {
+  const dim3 grid(ceil_div(L_v, kColKeys), H, B);
+  const int n_pad = mask_n_pad(ceil_div(L_v, block));
+  if (kbar != nullptr)
+    hipLaunchKernelGGL((a2v_colmass_kernel<D, true>), grid, dim3(kXNT), 0, s, q_a, k_v, lse2,
+                       colmass, H, L_v, L_a, c, kbar, block, n_pad);
+  else
+    hipLaunchKernelGGL((a2v_colmass_kernel<D, false>), grid, dim3(kXNT), 0, s, q_a, k_v, lse2,
+                       colmass, H, L_v, L_a, c, kbar, block, n_pad);
+}
+
 template <int D>
 void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
                 const uint16_t* k_a, int B, int H, int L_v, int L_a, float scale,
                 int block, float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
-                int accumulate, char* ws, hipStream_t s) {
+                int accumulate, double* qbar, double* kbar, char* ws, hipStream_t s) {
   const CrossWs lay = cross_ws_layout(B, H, L_v, L_a);
   const float c = scale * kLog2e;
   const int P = B * H;
@@ -649,8 +891,7 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
   const size_t nlse = static_cast<size_t>(P) * L_a;
   hipLaunchKernelGGL(lse_combine_kernel, dim3((nlse + 63) / 64), dim3(64), 0, s,
                      lse_part, lse_a, P, L_a, nchunk);
-  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColKeys), H, B), dim3(kXNT),
-                     0, s, q_a, k_v, lse_a, colmass, H, L_v, L_a, c);
+  launch_a2v_colmass<D>(q_a, k_v, lse_a, colmass, B, H, L_v, L_a, c, kbar, block, s);
   const int n_b = ceil_div(L_v, block);
   hipLaunchKernelGGL(a2v_finalize_kernel, dim3(n_b, B), dim3(block), 0, s, colmass,
                      sal_v_tok, sal_v_blk, L_v, H,
@@ -660,7 +901,8 @@ void cross_bf16(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
     float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
     hipLaunchKernelGGL((v2a_colmass_kernel<D, false>), dim3(nchunk3, 1, P),
-                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, nullptr);
+                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, nullptr,
+                       qbar, block, mask_n_pad(ceil_div(L_v, block)));
     hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
                        v2a_part, v2a_head, L_a, nchunk3);
     const size_t na = static_cast<size_t>(B) * L_a;
@@ -685,8 +927,8 @@ template <int D>
 void cross_bf16_from_lse(const uint16_t* q_a, const uint16_t* k_v, const uint16_t* q_v,
                          const uint16_t* k_a, const float* lse_a, const float* lse_v, int B,
                          int H, int L_v, int L_a, float scale, int block, float* sal_v_tok,
-                         float* sal_v_blk, float* sal_a_tok, int accumulate, char* ws,
-                         hipStream_t s) {
+                         float* sal_v_blk, float* sal_a_tok, int accumulate, double* qbar,
+                         double* kbar, char* ws, hipStream_t s) {
   const CrossWs lay = cross_ws_layout(B, H, L_v, L_a);
   const float c = scale * kLog2e;
   const int P = B * H;
@@ -696,8 +938,7 @@ void cross_bf16_from_lse(const uint16_t* q_a, const uint16_t* k_v, const uint16_
   const size_t cblocks = (nlse + 255) / 256;
   hipLaunchKernelGGL(lse_to_log2_kernel, dim3(static_cast<unsigned>(cblocks < 1024 ? cblocks : 1024)),
                      dim3(256), 0, s, lse_a, lse2, nlse);
-  hipLaunchKernelGGL(a2v_colmass_kernel<D>, dim3(ceil_div(L_v, kColKeys), H, B), dim3(kXNT),
-                     0, s, q_a, k_v, lse2, colmass, H, L_v, L_a, c);
+  launch_a2v_colmass<D>(q_a, k_v, lse2, colmass, B, H, L_v, L_a, c, kbar, block, s);
   const int n_b = ceil_div(L_v, block);
   hipLaunchKernelGGL(a2v_finalize_kernel, dim3(n_b, B), dim3(block), 0, s, colmass,
                      sal_v_tok, sal_v_blk, L_v, H,
@@ -707,7 +948,8 @@ void cross_bf16_from_lse(const uint16_t* q_a, const uint16_t* k_v, const uint16_
     const int nchunk3 = ceil_div(L_v, kV2aChunk);
     float* v2a_head = reinterpret_cast<float*>(ws + lay.v2a_head);
     hipLaunchKernelGGL((v2a_colmass_kernel<D, true>), dim3(nchunk3, 1, P),
-                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, lse_v);
+                       dim3(kXNT), 0, s, q_v, k_a, v2a_part, L_v, L_a, nchunk3, c, lse_v,
+                       qbar, block, mask_n_pad(ceil_div(L_v, block)));
     hipLaunchKernelGGL(v2a_chunk_sum_kernel, dim3(ceil_div(L_a, 64), P), dim3(256), 0, s,
                        v2a_part, v2a_head, L_a, nchunk3);
     const size_t na = static_cast<size_t>(B) * L_a;
@@ -758,14 +1000,14 @@ void launch_cross_scores_bf16(const uint16_t* q_a, const uint16_t* k_v,
                               const uint16_t* q_v, const uint16_t* k_a, int B,
                               int H, int L_v, int L_a, int d, float scale,
                               int block, float* sal_v_tok, float* sal_v_blk,
-                              float* sal_a_tok, int accumulate, char* ws,
-                              hipStream_t s) {
+                              float* sal_a_tok, int accumulate, double* qbar,
+                              double* kbar, char* ws, hipStream_t s) {
   if (d == 128)
     cross_bf16<128>(q_a, k_v, q_v, k_a, B, H, L_v, L_a, scale, block, sal_v_tok,
-                    sal_v_blk, sal_a_tok, accumulate, ws, s);
+                    sal_v_blk, sal_a_tok, accumulate, qbar, kbar, ws, s);
   else
     cross_bf16<64>(q_a, k_v, q_v, k_a, B, H, L_v, L_a, scale, block, sal_v_tok,
-                   sal_v_blk, sal_a_tok, accumulate, ws, s);
+                   sal_v_blk, sal_a_tok, accumulate, qbar, kbar, ws, s);
 }
 
 void launch_cross_scores_from_lse_bf16(const uint16_t* q_a, const uint16_t* k_v,
@@ -773,13 +1015,14 @@ void launch_cross_scores_from_lse_bf16(const uint16_t* q_a, const uint16_t* k_v,
                                        const float* lse_a, const float* lse_v, int B, int H,
                                        int L_v, int L_a, int d, float scale, int block,
                                        float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
-                                       int accumulate, char* ws, hipStream_t s) {
+                                       int accumulate, double* qbar, double* kbar,
+                                       char* ws, hipStream_t s) {
   if (d == 128)
     cross_bf16_from_lse<128>(q_a, k_v, q_v, k_a, lse_a, lse_v, B, H, L_v, L_a, scale, block,
-                             sal_v_tok, sal_v_blk, sal_a_tok, accumulate, ws, s);
+                             sal_v_tok, sal_v_blk, sal_a_tok, accumulate, qbar, kbar, ws, s);
   else
     cross_bf16_from_lse<64>(q_a, k_v, q_v, k_a, lse_a, lse_v, B, H, L_v, L_a, scale, block,
-                            sal_v_tok, sal_v_blk, sal_a_tok, accumulate, ws, s);
+                            sal_v_tok, sal_v_blk, sal_a_tok, accumulate, qbar, kbar, ws, s);
 }
 
 void launch_cross_scores_f32(const float* q_a, const float* k_v,

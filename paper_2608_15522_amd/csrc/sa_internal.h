@@ -162,8 +162,8 @@ void launch_cross_scores_bf16(const uint16_t* q_a, const uint16_t* k_v,
                               const uint16_t* q_v, const uint16_t* k_a, int B,
                               int H, int L_v, int L_a, int d, float scale,
                               int block, float* sal_v_tok, float* sal_v_blk,
-                              float* sal_a_tok, int accumulate, char* ws,
-                              hipStream_t s);
+                              float* sal_a_tok, int accumulate, double* qbar,
+                              double* kbar, char* ws, hipStream_t s);
 // Saliency from the row LSEs (natural log, [B,H,L_a] and [B,H,L_v]) of the
 // two cross-attention forwards; the workspace is cross_ws_layout's.
 void launch_cross_scores_from_lse_bf16(const uint16_t* q_a, const uint16_t* k_v,
@@ -171,7 +171,8 @@ void launch_cross_scores_from_lse_bf16(const uint16_t* q_a, const uint16_t* k_v,
                                        const float* lse_a, const float* lse_v, int B, int H,
                                        int L_v, int L_a, int d, float scale, int block,
                                        float* sal_v_tok, float* sal_v_blk, float* sal_a_tok,
-                                       int accumulate, char* ws, hipStream_t s);
+                                       int accumulate, double* qbar, double* kbar, char* ws,
+                                       hipStream_t s);
 void launch_cross_scores_f32(const float* q_a, const float* k_v,
                              const float* q_v, const float* k_a, int B, int H,
                              int L_v, int L_a, int d, float scale, int block,
@@ -186,6 +187,15 @@ void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
                              int k_keep, const uint8_t* prot_flag,
                              int32_t* kv_idx, int32_t* kv_cnt, uint8_t* mask,
                              float* scores, char* ws, hipStream_t s);
+// The pooling pass alone (K5): block means of q_v and k_v into qbar, kbar
+// ([B,H,d,mask_n_pad(n_b)]).
+void launch_block_pool(const void* q_v, const void* k_v, int B, int H, int L_v, int d,
+                       int dtype, int block, double* qbar, double* kbar, hipStream_t s);
+// The mask from given block means (K6 alone).
+void launch_mask_from_means(const double* qbar, const double* kbar, int B, int H, int L_v,
+                            int d, float scale, int block, int k_keep,
+                            const uint8_t* prot_flag, int32_t* kv_idx, int32_t* kv_cnt,
+                            uint8_t* mask, float* scores, hipStream_t s);
 void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
                                   const uint16_t* v, uint16_t* o, float* lse,
                                   int B, int H, int L, int d, float scale,

@@ -432,18 +432,11 @@ void launch_select_protected(const float* sal_blk, int B, int n_b, int k_prot,
                      k_prot, n_pad, prot_idx, prot_flag);
 }
 
-void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
-                             int L_v, int d, int dtype, float scale, int block,
-                             int k_keep, const uint8_t* prot_flag,
-                             int32_t* kv_idx, int32_t* kv_cnt, uint8_t* mask,
-                             float* scores, char* ws, hipStream_t s) {
+void launch_block_pool(const void* q_v, const void* k_v, int B, int H, int L_v, int d,
+                       int dtype, int block, double* qbar, double* kbar, hipStream_t s) {
   const int n_b = ceil_div(L_v, block);
-  const int P = B * H;
-  const MaskWs lay = mask_ws_layout(B, H, n_b, d);
-  double* qbar = reinterpret_cast<double*>(ws + lay.qbar);
-  double* kbar = reinterpret_cast<double*>(ws + lay.kbar);
   const int n_pad = mask_n_pad(n_b);
-  const dim3 pgrid(ceil_div(n_b, kPoolBlocks), P);
+  const dim3 pgrid(ceil_div(n_b, kPoolBlocks), B * H);
   if (dtype == 0) {
     const uint16_t* q = static_cast<const uint16_t*>(q_v);
     const uint16_t* k = static_cast<const uint16_t*>(k_v);
@@ -463,7 +456,15 @@ void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
       hipLaunchKernelGGL((block_pool_kernel<float, 64>), pgrid, dim3(256), 0, s, q, k,
                          qbar, kbar, L_v, block, n_b, n_pad);
   }
-  const int E = n_pad / 64;
+}
+
+void launch_mask_from_means(const double* qbar, const double* kbar, int B, int H, int L_v,
+                            int d, float scale, int block, int k_keep,
+                            const uint8_t* prot_flag, int32_t* kv_idx, int32_t* kv_cnt,
+                            uint8_t* mask, float* scores, hipStream_t s) {
+  const int n_b = ceil_div(L_v, block);
+  const int P = B * H;
+  const int E = mask_n_pad(n_b) / 64;
   const dim3 mgrid(8 * ceil_div(P, 8) * ceil_div(n_b, mask_rows_per_wg(E)));
   const double sc = static_cast<double>(scale);
   if (d == 128)
@@ -472,6 +473,19 @@ void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
   else
     launch_mask_build<64>(E, mgrid, s, qbar, kbar, prot_flag, P, H, n_b, k_keep, sc, kv_idx,
                           kv_cnt, mask, scores);
+}
+
+void launch_build_block_mask(const void* q_v, const void* k_v, int B, int H,
+                             int L_v, int d, int dtype, float scale, int block,
+                             int k_keep, const uint8_t* prot_flag,
+                             int32_t* kv_idx, int32_t* kv_cnt, uint8_t* mask,
+                             float* scores, char* ws, hipStream_t s) {
+  const MaskWs lay = mask_ws_layout(B, H, ceil_div(L_v, block), d);
+  double* qbar = reinterpret_cast<double*>(ws + lay.qbar);
+  double* kbar = reinterpret_cast<double*>(ws + lay.kbar);
+  launch_block_pool(q_v, k_v, B, H, L_v, d, dtype, block, qbar, kbar, s);
+  launch_mask_from_means(qbar, kbar, B, H, L_v, d, scale, block, k_keep, prot_flag, kv_idx,
+                         kv_cnt, mask, scores, s);
 }
 
 }  // namespace sa

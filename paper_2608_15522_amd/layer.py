@@ -3,7 +3,9 @@
 ``LayerPlan`` allocates every output and workspace once (with torch), so a
 ``run()`` enqueues only the library's kernels: saliency (Eq. (1)-(2)),
 protected selection (Eq. (8)), protected block mask (Eq. (9)) and protected
-block-sparse attention (Eq. (10)/(11)).
+block-sparse attention (Eq. (10)/(11)).  ``run_pooled()`` is the same layer
+with the mask's block means (Eq. (6)) taken from the saliency streams
+(``sa_cross_scores_pooled`` + ``sa_build_block_mask_pooled``).
 """
 from __future__ import annotations
 
@@ -36,6 +38,9 @@ class LayerPlan:
                  for c in (sa.SA_CALL_CROSS_SCORES, sa.SA_CALL_BUILD_BLOCK_MASK,
                            sa.SA_CALL_SPARSE_ATTENTION))
         self.ws = e(max(ws, 1), dt=u8)
+        n_pad = sa.sa_pool_columns(n_b)
+        self.qbar = e(B, H, d, n_pad, dt=torch.float64) if with_audio else None
+        self.kbar = e(B, H, d, n_pad, dt=torch.float64) if with_audio else None
 
     def cross_scores(self, q_a, k_v, q_v, k_a):
         sa.sa_cross_scores(q_a, k_v, q_v if self.with_audio else None,
@@ -43,6 +48,14 @@ class LayerPlan:
                            self.block, sal_v_tok=self.sal_v_tok,
                            sal_v_blk=self.sal_v_blk, sal_a_tok=self.sal_a_tok,
                            ws=self.ws)
+
+    def cross_scores_pooled(self, q_a, k_v, q_v, k_a, lse_a=None, lse_v=None):
+        """The saliency (standalone, or from the forwards' row LSEs) and the
+        block means of Q^v and K^v into qbar, kbar."""
+        sa.sa_cross_scores_pooled(q_a, k_v, q_v, k_a, self.scale, self.block,
+                                  lse_a=lse_a, lse_v=lse_v, sal_v_tok=self.sal_v_tok,
+                                  sal_v_blk=self.sal_v_blk, sal_a_tok=self.sal_a_tok,
+                                  qbar=self.qbar, kbar=self.kbar, ws=self.ws)
 
     def select_protected(self):
         sa.sa_select_protected(self.sal_v_blk, self.k_prot,
@@ -54,6 +67,11 @@ class LayerPlan:
                                self.prot_flag, kv_idx=self.kv_idx,
                                kv_cnt=self.kv_cnt, ws=self.ws)
 
+    def build_block_mask_pooled(self):
+        sa.sa_build_block_mask_pooled(self.qbar, self.kbar, self.L_v, self.scale, self.block,
+                                      self.k_keep, self.prot_flag, kv_idx=self.kv_idx,
+                                      kv_cnt=self.kv_cnt)
+
     def sparse_attention(self, q_v, k_v, v_v):
         sa.sa_sparse_attention(q_v, k_v, v_v, self.scale, self.block,
                                self.kv_idx, self.kv_cnt, o=self.o, lse=self.lse,
@@ -63,6 +81,13 @@ class LayerPlan:
         self.cross_scores(q_a, k_v, q_v, k_a)
         self.select_protected()
         self.build_block_mask(q_v, k_v)
+        self.sparse_attention(q_v, k_v, v_v)
+        return self.o
+
+    def run_pooled(self, q_v, k_v, v_v, q_a, k_a):
+        self.cross_scores_pooled(q_a, k_v, q_v, k_a)
+        self.select_protected()
+        self.build_block_mask_pooled()
         self.sparse_attention(q_v, k_v, v_v)
         return self.o
 

@@ -85,6 +85,21 @@ bool dispatch(const std::string& name, size_t a, int* rc) {
                                    I(a + 9), I(a + 10), I(a + 11), F(a + 12), I(a + 13),
                                    Pt<float>(a + 14), Pt<float>(a + 15), Pt<float>(a + 16),
                                    I(a + 17), P(a + 18), Z(a + 19), P(a + 20));
+  } else if (name == "sa_cross_scores_pooled") {
+    need(23);
+    *rc = sa_cross_scores_pooled(P(a), P(a + 1), P(a + 2), P(a + 3), Pt<const float>(a + 4),
+                                 Pt<const float>(a + 5), I(a + 6), I(a + 7), I(a + 8),
+                                 I(a + 9), I(a + 10), I(a + 11), F(a + 12), I(a + 13),
+                                 Pt<float>(a + 14), Pt<float>(a + 15), Pt<float>(a + 16),
+                                 I(a + 17), Pt<double>(a + 18), Pt<double>(a + 19), P(a + 20),
+                                 Z(a + 21), P(a + 22));
+  } else if (name == "sa_build_block_mask_pooled") {
+    need(15);
+    *rc = sa_build_block_mask_pooled(Pt<const double>(a), Pt<const double>(a + 1), I(a + 2),
+                                     I(a + 3), I(a + 4), I(a + 5), F(a + 6), I(a + 7),
+                                     I(a + 8), Pt<const uint8_t>(a + 9), Pt<int32_t>(a + 10),
+                                     Pt<int32_t>(a + 11), Pt<uint8_t>(a + 12),
+                                     Pt<float>(a + 13), P(a + 14));
   } else if (name == "sa_select_protected") {
     need(7);
     *rc = sa_select_protected(Pt<const float>(a), I(a + 1), I(a + 2), I(a + 3),

@@ -28,11 +28,11 @@ void launch_protected_token_attention_f32(const float*, const float*, const floa
                                           int, hipStream_t) SA_STUB()
 void launch_cross_scores_bf16(const uint16_t*, const uint16_t*, const uint16_t*,
                               const uint16_t*, int, int, int, int, int, float, int, float*,
-                              float*, float*, int, char*, hipStream_t) SA_STUB()
+                              float*, float*, int, double*, double*, char*, hipStream_t) SA_STUB()
 void launch_cross_scores_from_lse_bf16(const uint16_t*, const uint16_t*, const uint16_t*,
                                        const uint16_t*, const float*, const float*, int, int,
                                        int, int, int, float, int, float*, float*, float*, int,
-                                       char*, hipStream_t) SA_STUB()
+                                       double*, double*, char*, hipStream_t) SA_STUB()
 void launch_cross_scores_f32(const float*, const float*, const float*, const float*, int, int,
                              int, int, int, float, int, float*, float*, float*, int, char*,
                              hipStream_t) SA_STUB()
@@ -41,6 +41,11 @@ void launch_select_protected(const float*, int, int, int, int32_t*, uint8_t*,
 void launch_build_block_mask(const void*, const void*, int, int, int, int, int, float, int, int,
                              const uint8_t*, int32_t*, int32_t*, uint8_t*, float*, char*,
                              hipStream_t) SA_STUB()
+void launch_block_pool(const void*, const void*, int, int, int, int, int, int, double*, double*,
+                       hipStream_t) SA_STUB()
+void launch_mask_from_means(const double*, const double*, int, int, int, int, float, int, int,
+                            const uint8_t*, int32_t*, int32_t*, uint8_t*, float*,
+                            hipStream_t) SA_STUB()
 void launch_sparse_attention_bf16(const uint16_t*, const uint16_t*, const uint16_t*, uint16_t*,
                                   float*, int, int, int, int, float, int, const int32_t*,
                                   const int32_t*, char*, hipStream_t) SA_STUB()

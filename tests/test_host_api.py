@@ -168,6 +168,17 @@ _xlse = _Call("sa_cross_scores_from_lse", q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE
              stream=None)
 
 
+_xpool = _Call("sa_cross_scores_pooled", q_a=FAKE, k_v=FAKE, q_v=FAKE, k_a=FAKE, lse_a=None, lse_v=None,
+               B=1, H=1, L_v=1000, L_a=64, d=128, dtype=0, scale=0.088, block=128,
+               sal_v_tok=None, sal_v_blk=FAKE, sal_a_tok=FAKE, accumulate=0, qbar=FAKE,
+               kbar=FAKE + (1 << 20), ws=FAKE, ws_bytes=1 << 40, stream=None)
+
+
+_mpool = _Call("sa_build_block_mask_pooled", qbar=FAKE, kbar=FAKE + (1 << 20), B=1, H=1, L_v=1000, d=128,
+               scale=0.088, block=128, k_keep=2, prot_flag=None, kv_idx=FAKE, kv_cnt=FAKE,
+               mask=None, scores=None, stream=None)
+
+
 _select = _Call("sa_select_protected", sal_blk=FAKE, B=1, n_b=8, k_prot=2, prot_idx=None, prot_flag=FAKE,
              stream=None)
 
@@ -278,6 +289,25 @@ INVALID = [
     (_cross, dict(sal_v_blk=None), sa.SA_ERR_INVALID_ARG, "sal_v_blk is NULL"),
     (_cross, dict(q_a=None), sa.SA_ERR_INVALID_ARG, "q_a is NULL"),
     (_cross, dict(ws_bytes=1), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_xpool, dict(lse_a=FAKE), sa.SA_ERR_INVALID_ARG, "lse_a and lse_v"),
+    (_xpool, dict(lse_a=FAKE, lse_v=FAKE, dtype=1), sa.SA_ERR_UNSUPPORTED, "SA_BF16"),
+    (_xpool, dict(q_v=None), sa.SA_ERR_INVALID_ARG, "q_v is NULL"),
+    (_xpool, dict(sal_a_tok=None), sa.SA_ERR_INVALID_ARG, "sal_a_tok is NULL"),
+    (_xpool, dict(qbar=None), sa.SA_ERR_INVALID_ARG, "qbar is NULL"),
+    (_xpool, dict(kbar=FAKE + 4), sa.SA_ERR_INVALID_ARG, "aligned"),
+    # 1 x 1 x 128 x 64 doubles (64 KB) each: kbar 32 KB after qbar overlaps it
+    (_xpool, dict(kbar=FAKE + 32 * 1024), sa.SA_ERR_INVALID_ARG, "overlap"),
+    (_xpool, dict(L_a=0), sa.SA_ERR_INVALID_ARG, "L_a=0"),
+    (_xpool, dict(accumulate=3), sa.SA_ERR_INVALID_ARG, "accumulate"),
+    (_xpool, dict(block=32), sa.SA_ERR_UNSUPPORTED, "block"),
+    (_xpool, dict(ws_bytes=4), sa.SA_ERR_WORKSPACE, "workspace"),
+    (_mpool, dict(k_keep=0), sa.SA_ERR_INVALID_ARG, "k_keep"),
+    (_mpool, dict(k_keep=9), sa.SA_ERR_INVALID_ARG, "k_keep"),
+    (_mpool, dict(qbar=None), sa.SA_ERR_INVALID_ARG, "qbar is NULL"),
+    (_mpool, dict(kbar=MISALIGNED), sa.SA_ERR_INVALID_ARG, "aligned"),
+    (_mpool, dict(kv_cnt=None), sa.SA_ERR_INVALID_ARG, "kv_cnt is NULL"),
+    (_mpool, dict(d=96), sa.SA_ERR_UNSUPPORTED, "head dim"),
+    (_mpool, dict(L_v=2049 * 128), sa.SA_ERR_UNSUPPORTED, "n_b"),
     (_select, dict(k_prot=-1), sa.SA_ERR_INVALID_ARG, "k_prot"),
     (_select, dict(k_prot=9), sa.SA_ERR_INVALID_ARG, "k_prot"),
     (_select, dict(n_b=0), sa.SA_ERR_INVALID_ARG, "n_b"),
@@ -293,6 +323,15 @@ def test_invalid_arguments_are_rejected(call, kw, code, needle):
     assert rc == code
     msg = sa.sa_last_error()
     assert needle in msg, msg
+
+
+def test_pool_columns():
+    """The pooled means are padded to the mask's row width: 64 * E with E the
+    smallest of 1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32 covering n_b."""
+    widths = [1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32]
+    for n_b in (1, 16, 64, 65, 256, 257, 384, 591, 640, 641, 1024, 1537, 2048):
+        assert sa.sa_pool_columns(n_b) == 64 * min(e for e in widths if 64 * e >= n_b)
+    assert sa.sa_pool_columns(0) == 0 and sa.sa_pool_columns(2049) == 0
 
 
 def test_empty_token_calls_launch_nothing():

@@ -12,7 +12,7 @@ import subprocess
 import pytest
 
 import paper_2608_15522_amd as sa
-from test_host_api import INVALID, _attn, _mask, _select
+from test_host_api import INVALID, _attn, _mask, _mpool, _select, _xpool
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HERE = os.path.join(ROOT, "tests", "host_asan")
@@ -80,7 +80,8 @@ def test_valid_calls_reach_the_launchers_under_sanitizers(checker):
     """Accepted arguments pass validation and reach the (stand-in) launcher;
     the return code then reflects the launch check of a machine without a
     GPU, so only the message is not checked."""
-    ok = [(_attn, {}), (_mask, {}), (_select, {}),
+    ok = [(_attn, {}), (_mask, {}), (_select, {}), (_xpool, {}), (_mpool, {}),
+          (_xpool, dict(dtype=1)),
           (_attn, dict(B=2, H=24, L=75600, ws_bytes=1 << 20))]
     lines = [f"call {c.name} 0 - " + " ".join(_arg(v) for v in c.args(**kw)) for c, kw in ok]
     res = _run(checker, lines)
