@@ -66,6 +66,10 @@ def parse():
     p.add_argument("--no-cross-attention", action="store_true",
                    help="skip timing the cross-modal attention forwards and the saliency "
                         "from their LSEs")
+    p.add_argument("--layer", choices=("plain", "pooled"), default="plain",
+                   help="the timed layer: the four calls of the boundary (plain), or the "
+                        "same steps with the mask's block means pooled inside the saliency "
+                        "streams (pooled)")
     p.add_argument("--no-pooled", action="store_true",
                    help="skip the layer with the block means pooled inside the saliency "
                         "streams")
@@ -123,27 +127,38 @@ def computed_flops(kv_idx, kv_cnt, L, block, d):
     return 4 * d * total
 
 
-def time_layer(plan, t, steps, warmup, torch):
+def time_layer(plan, t, steps, warmup, torch, pooled=False):
+    """The four calls of one layer, HIP events between them.  pooled: the
+    layer with the mask's block means pooled inside the saliency streams."""
+    run = plan.run_pooled if pooled else plan.run
     for _ in range(warmup):
-        plan.run(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+        run(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     t0 = time.perf_counter()
     for i in range(steps):
         e = ev[i]
         e[0].record()
-        plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        if pooled:
+            plan.cross_scores_pooled(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
+        else:
+            plan.cross_scores(t["q_a"], t["k_v"], t["q_v"], t["k_a"])
         e[1].record()
         plan.select_protected()
         e[2].record()
-        plan.build_block_mask(t["q_v"], t["k_v"])
+        if pooled:
+            plan.build_block_mask_pooled()
+        else:
+            plan.build_block_mask(t["q_v"], t["k_v"])
         e[3].record()
         plan.sparse_attention(t["q_v"], t["k_v"], t["v_v"])
         e[4].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    names = ["sa_cross_scores", "sa_select_protected", "sa_build_block_mask",
-             "sa_sparse_attention"]
+    names = (["sa_cross_scores_pooled", "sa_select_protected", "sa_build_block_mask_pooled",
+              "sa_sparse_attention"] if pooled else
+             ["sa_cross_scores", "sa_select_protected", "sa_build_block_mask",
+              "sa_sparse_attention"])
     per_call = {n: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps)) / steps
                 for j, n in enumerate(names)}
     med = {n: sorted(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(steps))[steps // 2]
@@ -657,7 +672,8 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    ms_layer, per_call, per_call_median = time_layer(plan, t, args.steps, args.warmup, torch)
+    ms_layer, per_call, per_call_median = time_layer(plan, t, args.steps, args.warmup, torch,
+                                                     pooled=args.layer == "pooled")
     print(f"bench: layer {ms_layer:.3f} ms {per_call}", file=sys.stderr, flush=True)
 
     kv_idx = plan.kv_idx.cpu().numpy()
@@ -681,7 +697,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded Gaussian Q/K/V with planted audio-correlated video blocks)",
-        "config": {"workload": w.name, "B": w.B, "H": w.H, "L_v": w.L_v, "L_a": w.L_a,
+        "config": {"workload": w.name, "layer": args.layer, "B": w.B, "H": w.H, "L_v": w.L_v, "L_a": w.L_a,
                    "d": w.d, "block": w.block, "density": w.density, "k_keep": w.k_keep,
                    "k_prot": w.k_prot, "n_b": n_b},
         "per_call_ms": {k: round(v, 4) for k, v in per_call.items()},
