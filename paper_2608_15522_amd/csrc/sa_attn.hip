@@ -46,26 +46,42 @@ constexpr int kTile = 64;       // keys per LDS tile
 constexpr int kCusPerXcd = 32;  // MI355X: 8 XCDs of 32 CUs
 
 // Query blocks of every (b,h) pair ordered by kv_cnt descending, then by
-// block index ascending.
-__global__ void __launch_bounds__(256)
+// block index ascending.  Each block gets the key (n_b - cnt) * 4096 + index,
+// unique and in that order, and its rank is the number of smaller keys.
+// Grid (pairs, ceil(n_b / kOrderRows)): every workgroup loads the pair's keys
+// into LDS and ranks kOrderRows of its blocks, reading the keys four at a time
+// (entries past n_b hold INT_MAX and never count).
+constexpr int kOrderRows = 256;
+__global__ void __launch_bounds__(kOrderRows)
 order_rows_kernel(const int32_t* __restrict__ kv_cnt, int32_t* __restrict__ order,
                   int n_b) {
-  __shared__ int cnt[kMaxBlocks];
+  __shared__ __attribute__((aligned(16))) int key[kMaxBlocks];
   const size_t base = static_cast<size_t>(blockIdx.x) * n_b;
-  for (int r = threadIdx.x; r < n_b; r += blockDim.x) {
-    int c = kv_cnt[base + r];
-    cnt[r] = c < 0 ? 0 : (c > n_b ? n_b : c);
+  const int n4 = ceil_div(n_b, 4);
+  for (int r = threadIdx.x; r < 4 * n4; r += blockDim.x) {
+    int k = 0x7fffffff;
+    if (r < n_b) {
+      int c = kv_cnt[base + r];
+      c = c < 0 ? 0 : (c > n_b ? n_b : c);
+      k = (n_b - c) * 4096 + r;
+    }
+    key[r] = k;
   }
   __syncthreads();
-  for (int r = threadIdx.x; r < n_b; r += blockDim.x) {
-    const int mine = cnt[r];
-    int rank = 0;
-    for (int j = 0; j < n_b; ++j) {
-      const int o = cnt[j];
-      rank += (o > mine) || (o == mine && j < r);
-    }
-    order[base + rank] = r;
+  const int r = blockIdx.y * kOrderRows + threadIdx.x;
+  if (r >= n_b) return;
+  const int mine = key[r];
+  const int4* k4 = reinterpret_cast<const int4*>(key);
+  int rk[4] = {0, 0, 0, 0};
+#pragma unroll 4
+  for (int j4 = 0; j4 < n4; ++j4) {
+    const int4 o = k4[j4];
+    rk[0] += o.x < mine;
+    rk[1] += o.y < mine;
+    rk[2] += o.z < mine;
+    rk[3] += o.w < mine;
   }
+  order[base + (rk[0] + rk[1]) + (rk[2] + rk[3])] = r;
 }
 
 // Launch schedule when the pair count is a multiple of 8.  Workgroup w runs
@@ -843,7 +859,8 @@ void launch_sparse_attention_bf16(const uint16_t* q, const uint16_t* k,
   int32_t* sched = reinterpret_cast<int32_t*>(ws + lay.sched);
   int* claim = reinterpret_cast<int*>(ws + lay.claim);
   const float c = scale * kLog2e;
-  hipLaunchKernelGGL(order_rows_kernel, dim3(P), dim3(256), 0, s, kv_cnt, order, n_b);
+  hipLaunchKernelGGL(order_rows_kernel, dim3(P, ceil_div(n_b, kOrderRows)), dim3(kOrderRows), 0,
+                     s, kv_cnt, order, n_b);
   // pair count a multiple of 8: persistent workgroups, as many as the chip
   // holds at once (2 per CU, 32 CUs per XCD) and no more than the rows
   dim3 grid(P * n_b);
