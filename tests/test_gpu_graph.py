@@ -73,6 +73,35 @@ def test_layer_graph_replays_reproduce_the_eager_layer():
     _replays_match(graph, outputs, reference)
 
 
+def test_pooled_layer_graph_replays_reproduce_the_eager_layer():
+    """The same layer with the block means pooled inside the saliency streams
+    (sa_cross_scores_pooled + sa_build_block_mask_pooled)."""
+    w = W
+    k_keep, k_prot = max(1, w.n_b // 4), 2
+    print(f"case graph pooled layer B={w.B} H={w.H} L_v={w.L_v} n_b={w.n_b}", flush=True)
+    x = synth.make_inputs(w)
+    t = {k: to_dev(x[k], w.dtype) for k in ("q_v", "k_v", "v_v", "q_a", "k_a")}
+    plan = LayerPlan(w.B, w.H, w.L_v, w.L_a, w.d, w.block, k_keep, k_prot, w.scale,
+                     want_lse=True)
+
+    def layer():
+        plan.run_pooled(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+
+    layer()
+    torch.cuda.synchronize()
+    n_b = w.n_b
+    outputs = [plan.sal_v_tok, plan.sal_v_blk, plan.sal_a_tok, plan.prot_flag, plan.kv_idx,
+               plan.kv_cnt, plan.o, plan.lse, plan.qbar[..., :n_b], plan.kbar[..., :n_b]]
+    reference = [o.clone() for o in outputs]
+    # the eager pooled layer equals the plain one
+    plan.run(t["q_v"], t["k_v"], t["v_v"], t["q_a"], t["k_a"])
+    torch.cuda.synchronize()
+    for o, r in zip(outputs[:8], reference[:8]):
+        assert torch.equal(o.view(torch.uint8), r.view(torch.uint8))
+    graph = _capture(layer)
+    _replays_match(graph, outputs, reference)
+
+
 def test_audio_branch_graph_replays_reproduce_the_eager_branch():
     w = W
     print(f"case graph audio branch L_a={w.L_a} block_a={w.block_a} k_tok_a={w.k_tok_a}",
