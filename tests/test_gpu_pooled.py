@@ -31,6 +31,9 @@ CASES = [
                             L_a=700, n_plant=2)),
     # three audio slabs, L_v a multiple of 1024 (no tail)
     ("slabs3", BASE.with_(name="p4", H=2, frames=4, rows=16, cols=32, L_a=1100, n_plant=2)),
+    # shorter than one 64-key tile: one block, one partial unit, 7 audio tokens
+    ("tiny", BASE.with_(name="p5", H=1, d=64, block=64, frames=1, rows=5, cols=10, L_a=7,
+                        n_plant=0)),
     ("ovi", BASE),
     ("ltx", synth.WORKLOADS["ltx_bf16"]),
 ]
