@@ -215,7 +215,10 @@ int sa_build_block_mask(const void* q_v, const void* k_v, int B, int H,
  * both: sa_cross_scores_pooled writes them, sa_build_block_mask_pooled ranks
  * them.  The pair gives the same lists as sa_cross_scores (or
  * sa_cross_scores_from_lse) followed by sa_build_block_mask: the means are
- * exact fp64 sums of the bf16 (or fp32) inputs divided once, as there.
+ * fp64 sums of the bf16 (or fp32) inputs divided once, as there, and such a
+ * sum is exact (so independent of the order of the additions) whenever the
+ * values of a block lie within 2^44 (bf16) or 2^28 (fp32) of each other in
+ * magnitude.
  *
  * Layout of the means: qbar and kbar are each [B,H,d,n_pad] fp64 (block index
  * innermost), n_pad = sa_pool_columns(n_b); columns n_b .. n_pad-1 are never

@@ -311,22 +311,15 @@ struct ColAcc {
 // ---- block means fused into the streams (Sec. 4.2, Eq. (6)) ------------------
 // The mean of Q^v and of K^v over each block of `block` tokens (the last block
 // over its true length), written as [d][n_pad] per (b,h) like the mask call's
-// own pooling.  Sums of bf16 values are exact in fp64, so the means equal
-// that pooling bit for bit whatever the order of the additions.
+// own pooling.  A sum of at most 128 bf16 values (8 significant bits each) is
+// exact in fp64 whenever their magnitudes lie within 2^44 of each other, so
+// the means equal that pooling bit for bit whatever the order of the
+// additions, and are divided once.
 
 // 8 bf16 of a 16-byte chunk added to acc in fp64.
 __device__ __forceinline__ void add_bf16x8(u32x4 v, double (&acc)[8]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    acc[2 * i] += static_cast<double>(__uint_as_float(v[i] << 16));
-    acc[2 * i + 1] += static_cast<double>(__uint_as_float(v[i] & 0xffff0000u));
-  }
-}
-
-// 4 bf16 (8 bytes) added to acc in fp64.
-__device__ __forceinline__ void add_bf16x4(u32x2 v, double (&acc)[4]) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
     acc[2 * i] += static_cast<double>(__uint_as_float(v[i] << 16));
     acc[2 * i + 1] += static_cast<double>(__uint_as_float(v[i] & 0xffff0000u));
   }
@@ -371,9 +364,10 @@ __device__ __forceinline__ double dpp_row_sum(double x) {
 
 // Keys of a column-mass stream (K2), pooled from the LDS ring.  Lane l of
 // wave w takes d quarter q = 4w + l/16 (d = 4q .. 4q+3) of key rows l % 16 and
-// l % 16 + 16 of every 32-key unit, read while the unit's MFMAs run; at the end
-// of a block the 16 lanes that share q (one DPP row) add their sums
-// (dpp_row_sum), and the lane of row 0 writes the 4 means.  Waves past D/16 (d = 64) take no part.
+// l % 16 + 16 of every 32-key unit, read while the unit's MFMAs run; at the
+// end of a block the 16 lanes that share q (one DPP row) add their sums
+// (dpp_row_sum), and the lane of row 0 writes the 4 means.  Waves from D/16
+// on (at d = 64) take no part.
 template <int D>
 struct KeyPool {
   static constexpr int TB = KeyRing<D>::TB;

@@ -6,7 +6,7 @@
 //    the first k_prot.
 // K5 block_pool: per (b,h) and 8 consecutive blocks the mean of Q and of K
 //    over the valid tokens of each block, accumulated in fp64 (16-byte loads,
-//    fixed-order LDS reduction; the sums of bf16/fp32 inputs are exact),
+//    fixed-order LDS reduction; the sums are exact, see block_pool_kernel),
 //    stored as [d][n_pad] (block index innermost).
 // K6 mask_build (Sec. 4.2, Eq. (6) and (9)): per (b,h) and 16 query blocks
 //    (rows padded to 64 * E columns, E <= 10; 8 or 4 blocks for wider
@@ -72,8 +72,11 @@ template <> struct Elem<float> {
 constexpr int kMaxPoolBlock = 128;  // largest supported block
 
 // Grid (ceil(n_b / kPoolBlocks), P), 256 threads.  out[pair][:][c] (layout
-// [d][n_pad]) = mean of the rows of block c, in fp64: the sums of bf16 or
-// fp32 inputs are exact, the mean is rounded once.  Per block, thread
+// [d][n_pad]) = mean of the rows of block c, in fp64: a sum of at most 128
+// values is exact in fp64 whenever their magnitudes lie within 2^44 (bf16
+// inputs, 8 significant bits) or 2^28 (fp32, 24 bits) of each other, so the
+// result does not depend on the order of the additions, and the mean is
+// rounded once.  Per block, thread
 // (rg, cc) loads 16-byte chunk cc of rows rg, rg + RG, ... of both matrices
 // and the RG partial sums of each element are added in a fixed order; the
 // means of the workgroup's blocks are written as runs of consecutive
