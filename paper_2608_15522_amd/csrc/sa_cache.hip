@@ -83,8 +83,8 @@ __device__ __forceinline__ void rows_l1(const T* y, const T* yh, const uint8_t* 
     for (int u = 0; u < U; ++u) {
       const uint32_t j = j0 + u * kCacheThreads;
       const bool ok = j < n;
-      va[u] = ok ? ldg16(ya + static_cast<size_t>(j) * EPC) : u32x4{0u, 0u, 0u, 0u};
-      vb[u] = ok ? ldg16(yb + static_cast<size_t>(j) * EPC) : u32x4{0u, 0u, 0u, 0u};
+      va[u] = ok ? ldg16_nt(ya + static_cast<size_t>(j) * EPC) : u32x4{0u, 0u, 0u, 0u};
+      vb[u] = ok ? ldg16_nt(yb + static_cast<size_t>(j) * EPC) : u32x4{0u, 0u, 0u, 0u};
       pr[u] = flag != nullptr && ok && flag[r0 + j / cpr] != 0;
     }
 #pragma unroll

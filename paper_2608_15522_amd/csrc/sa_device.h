@@ -113,6 +113,13 @@ __device__ __forceinline__ void wait_vm() {
 __device__ __forceinline__ u32x4 ldg16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
+// The same load with the nontemporal cache policy (`nt`), for data that a
+// pass reads exactly once.  On gfx950 the block pooling's reads of Q^v and
+// K^v ran at about 6.1 TB/s with it against 5.0-5.4 TB/s without (same
+// kernel and box).
+__device__ __forceinline__ u32x4 ldg16_nt(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 __device__ __forceinline__ void stg16(void* p, u32x4 v) {
   *reinterpret_cast<u32x4*>(p) = v;
 }

@@ -111,7 +111,7 @@ block_pool_kernel(const T* __restrict__ q, const T* __restrict__ k,
 #pragma unroll
       for (int i = 0; i < NR; ++i) {
         const int r = rg + RG * i;
-        dst[which][i] = r < len ? ldg16(src + static_cast<size_t>(row0 + r) * D + cc * EPC)
+        dst[which][i] = r < len ? ldg16_nt(src + static_cast<size_t>(row0 + r) * D + cc * EPC)
                                 : u32x4{0u, 0u, 0u, 0u};
       }
     }
