@@ -15,9 +15,9 @@
 //    FMAs beyond (a few GFLOP per layer; fp32 would misrank scores closer
 //    than ~1e-6, and pooled-score gaps are that small), then per row
 //    either the full list (protected row) or the top-k_keep blocks: one
-//    wave finds the k-th smallest order key (value descending, index
-//    ascending) by a bitwise search with ballots and compacts the blocks at
-//    or below it into an ascending list.
+//    wave bounds the k-th smallest order key (value descending, index
+//    ascending) by halving a key range, counting with ballots, and compacts
+//    the blocks below the bound into an ascending list.
 #include "sa_device.h"
 #include "sa_internal.h"
 
@@ -182,31 +182,32 @@ __host__ __device__ constexpr int mask_rows_per_wg(int E) {
   return mask_uses_mfma(E) ? 16 : (E >= 20 ? 4 : 8);
 }
 
-// k-th smallest (1-based, 1 <= k <= number of keys) of the E x 64 distinct
-// keys held by one wave (E per lane).  Bits are fixed from the top; each step
-// counts the keys that share the fixed prefix and have a 0 next.  The search
-// stops once a single key shares the prefix: then key <= (k-th smallest)
-// exactly when (key & fixed) <= prefix, which is what the caller tests.
+// Bound of the k smallest (1 <= k <= number of real keys) of the E x 64 keys
+// held by one wave (E per lane): returns T such that exactly k keys are < T.
+// Real keys are distinct; padding keys are ~0 and never below a real one.
+// The search halves a key range [lo, lo + 2^w) that holds the k-th smallest
+// key: one compare per key against the midpoint, counted with ballots, tells
+// which half holds it.  It stops once the range holds that key alone.
 template <int E>
-__device__ __forceinline__ void wave_kth_prefix(const uint64_t* keys, int k, uint64_t& prefix,
-                                                uint64_t& fixed) {
-  prefix = 0;
-  fixed = 0;
-  int below = 0, size = 64 * E;  // keys below the prefix / sharing it
-  for (int bit = 63; bit >= 0 && size > 1; --bit) {
-    const uint64_t sel = fixed | (1ull << bit);
-    int cnt = 0;
+__device__ __forceinline__ uint64_t wave_kth_bound(const uint64_t* keys, int k) {
+  uint64_t lo = 0;
+  int below = 0, size = 64 * E;  // keys below lo / in the range
+  int w = 64;
+  do {
+    --w;
+    const uint64_t mid = lo | (1ull << w);
+    int cnt = 0;  // keys below mid
 #pragma unroll
-    for (int e = 0; e < E; ++e) cnt += __popcll(__ballot((keys[e] & sel) == prefix));
-    if (below + cnt < k) {
-      below += cnt;
-      size -= cnt;
-      prefix |= 1ull << bit;
+    for (int e = 0; e < E; ++e) cnt += __popcll(__ballot(keys[e] < mid));
+    if (cnt < k) {
+      size -= cnt - below;
+      below = cnt;
+      lo = mid;
     } else {
-      size = cnt;
+      size = cnt - below;
     }
-    fixed = sel;
-  }
+  } while (w > 0 && size > 1);
+  return lo + (1ull << w);
 }
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
@@ -375,14 +376,12 @@ mask_build_kernel(const double* __restrict__ qbar, const double* __restrict__ kb
       if (lane == 0) kv_cnt[row] = n_b;
       continue;
     }
-    uint64_t prefix, fixed;
-    wave_kth_prefix<E>(keys, k_keep, prefix, fixed);
+    const uint64_t bound = wave_kth_bound<E>(keys, k_keep);
     int base = 0;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int col = 64 * e + lane;
-      // padding keys (~0) never pass: the k-th key is a real one
-      const bool on = (keys[e] & fixed) <= prefix;
+      const bool on = keys[e] < bound;  // padding keys (~0) never pass
       const uint64_t m = __ballot(on);
       if (on) out_idx[base + __popcll(m & below_mask)] = col;
       base += __popcll(m);
