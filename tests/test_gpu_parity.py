@@ -1,6 +1,8 @@
 """GPU parity of the four C-ABI calls against the fp64 oracle, on seeded
 synthetic inputs.  Small shapes span several tiles and ragged tails and are
 compared element by element; edge cases use hand-built lists."""
+import functools
+
 import numpy as np
 import pytest
 import torch
@@ -278,3 +280,31 @@ def test_block_mask_at_padded_widths(n_b, E):
     assert np.all(np.abs(sc - G) <= 2.0 ** -24 * np.abs(G) + 1e-12)
     check_kv_lists(kv_idx.cpu().numpy(), kv_cnt.cpu().numpy(), prot, G, k_keep,
                    mask.cpu().numpy())
+
+
+@functools.lru_cache(maxsize=1)
+def _mask_case(n_b):
+    w = BASE.with_(name=f"x{n_b}", H=2, d=64, block=64, frames=1, rows=1,
+                   cols=64 * n_b - 5, L_a=16, n_plant=2)
+    x = synth.make_inputs(w)
+    return w, x, oracle.pooled_scores(x["q_v"], x["k_v"], w.scale, w.block)
+
+
+# the k-th order key is bounded by halving a key range; its extremes: the
+# smallest key alone, all but the largest, and every key (the bound then lies
+# between the largest real key and the padding keys of the row)
+@pytest.mark.parametrize("n_b,k_keep", [(64, 1), (64, 63), (64, 64), (600, 1), (600, 599),
+                                        (600, 600), (2000, 1), (2000, 1999), (2000, 2000)])
+def test_block_mask_kth_extremes(n_b, k_keep):
+    print(f"case mask k-th extremes n_b={n_b} k_keep={k_keep}", flush=True)
+    w, x, G = _mask_case(n_b)
+    assert w.n_b == n_b
+    t = {k: to_dev(x[k], "bf16") for k in ("q_v", "k_v")}
+    kv_idx, kv_cnt, mask, _ = sa.sa_build_block_mask(
+        t["q_v"], t["k_v"], w.scale, w.block, k_keep, None, want_mask=True)
+    torch.cuda.synchronize()
+    idx, cnt = kv_idx.cpu().numpy(), kv_cnt.cpu().numpy()
+    assert np.all(cnt == k_keep)
+    check_kv_lists(idx, cnt, np.zeros((1, n_b), dtype=np.uint8), G, k_keep, mask.cpu().numpy())
+    if k_keep == n_b:
+        assert np.array_equal(idx, np.broadcast_to(np.arange(n_b, dtype=np.int32), idx.shape))
