@@ -510,8 +510,11 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     wait_dma();
     __syncthreads();
   };
-  // Steady-state iteration for t + 2 < T_full (tiles t, t+1 and t+2 hold 64
-  // keys each).  The issue order is fixed by scheduling barriers so that
+  // Steady-state iteration: tiles t, t+1 and t+2 hold 64 keys each, with the
+  // copy indices t+1 and t+2 clamped to the last tile (a list without a tail
+  // tile runs every iteration here; past its end the last tile is copied
+  // again into the free buffer, and S(t+1) of the last iteration is
+  // discarded).  The issue order is fixed by scheduling barriers so that
   // every MFMA is followed by a share of the VALU work: in the QK^T phase
   // (S(t+1) into n0/n1) one bf16 pair of P(t) per MFMA; in the PV phase the
   // row sums of P(t), then the row max of S(t+1).  Operand reads run two
@@ -520,8 +523,8 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
 #pragma unroll
   for (int i = 0; i < NI; ++i) dma_full[i] = static_cast<uint32_t>(dma_row[i] * (D * 2)) + dma_col[i];
   auto main_iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
-    const char* kbase = kh + static_cast<size_t>(tile_key0(t + 2)) * D * 2;
-    const char* vbase = vh + static_cast<size_t>(tile_key0(t + 1)) * D * 2;
+    const char* kbase = kh + static_cast<size_t>(tile_key0(min(t + 2, T - 1))) * D * 2;
+    const char* vbase = vh + static_cast<size_t>(tile_key0(min(t + 1, T - 1))) * D * 2;
     const float mx = max_halves(mx_cur) * c;
     if (__any(mx > m + kRescaleSlack)) {
       const float m_new = fmaxf(m, mx);
@@ -657,7 +660,9 @@ sparse_attn_bf16_kernel(const uint16_t* __restrict__ q,
     __syncthreads();
   };
 
-  const int T_main = T_full > 2 ? T_full - 2 : 0;
+  // With a tail tile (T_full < T), its copies (row clamp) and its masked P
+  // take the generic iterations, from the one that first copies it.
+  const int T_main = T_full == T ? T : (T_full > 2 ? T_full - 2 : 0);
   int t = 0;
   for (; t + 1 < T_main; t += 2) {
     main_iter(t, sc0, sc1, sn_0, sn_1);
